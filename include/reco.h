@@ -1,0 +1,210 @@
+/*
+ * reco.h -- C ABI of the MI355X (gfx950) hot path of reward-coordinated
+ * KV-cache compression and decoding.
+ *
+ * The method (Section 3 of the paper) runs, after every completed reasoning
+ * step, a compression of the accumulated KV cache whose size is set by the
+ * step's process reward (Section 3.2), and controls the following generation
+ * with a reward-banded reflection-token penalty and an answer-perplexity stop
+ * rule (Section 3.3).  This library implements the data-parallel kernels of
+ * that loop:
+ *
+ *   reco_score           window attention mass of every cached key   (Eq. 2)
+ *   reco_select_compact  keep the top-m keys plus the window, compact
+ *                        the K/V rows in place                       (Sec. 3.2)
+ *   reco_decode_attn     GQA decode attention over the ragged,
+ *                        compacted cache (optionally appending the
+ *                        new token first)                            (Sec. 1, 3.2)
+ *   reco_logit_penalty   banded reflection-token logit penalty       (Eq. 3, 4)
+ *   reco_answer_ppl      answer perplexity and stop flag             (Eq. 5, 6)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Every pointer is a DEVICE pointer unless marked [host].  The caller owns
+ *   all memory and keeps it alive until the work on `stream` has finished.
+ * - Calls are asynchronous on `stream`; none synchronises, allocates device
+ *   memory or keeps state between calls.  Calls that take a workspace need
+ *   `ws_bytes >= reco_*_workspace_size(...)`; workspace contents need not be
+ *   initialised and are clobbered.
+ * - Host-side validation runs first: a call that returns anything other
+ *   than RECO_OK has launched nothing and changed nothing.
+ * - Device-side precondition failures (an append past capacity, a retention
+ *   outside (0, 1], a NaN or negative score, a token id out of range, a
+ *   stored length outside [0, capacity]) are reported through the optional
+ *   `dev_err` word: the first failing code is stored with an atomic
+ *   compare-and-swap from 0, so the caller should zero it before a call and
+ *   read it after synchronising.  A failing unit is left unchanged (select /
+ *   compact) or computed on clamped indices (decode); the call still returns
+ *   RECO_OK because the host cannot see device data.
+ * - KV cache layout: K and V are each
+ *       [n_layers][batch][n_kv_heads][capacity][head_dim]
+ *   in the cache dtype (fp32 or bf16), row-major; one (layer, sequence,
+ *   kv head) "unit" is a contiguous block of `capacity` rows.  `len`
+ *   ([n_layers][batch][n_kv_heads], int32) holds the number of valid rows of
+ *   each unit; rows at or beyond len are never read as keys.
+ * - GQA: query head hq (0 <= hq < n_q_heads) attends through KV head
+ *   hq / G with G = n_q_heads / n_kv_heads (1 <= G <= 16).
+ * - A call covers layers [layer0, layer0 + n_layers) of the cache; per-layer
+ *   inputs and outputs (queries, scores, outputs) are laid out with a
+ *   leading [n_layers] dimension for exactly those layers.
+ */
+#ifndef RECO_H
+#define RECO_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RECO_ABI_VERSION 1
+
+typedef enum reco_status {
+  RECO_OK = 0,
+  RECO_ERR_INVALID_ARG = 1,   /* null pointer, bad size, bad layer range ... */
+  RECO_ERR_UNSUPPORTED = 2,   /* valid but not implemented (head_dim, G, dtype) */
+  RECO_ERR_WORKSPACE = 3,     /* ws is null or smaller than required */
+  RECO_ERR_HIP = 4            /* a HIP launch failed */
+} reco_status_t;
+
+typedef enum reco_dtype { RECO_F32 = 0, RECO_BF16 = 1 } reco_dtype_t;
+
+/* Codes stored into *dev_err by kernels (first one wins). */
+enum {
+  RECO_DEV_OK = 0,
+  RECO_DEV_APPEND_OVERFLOW = 1,  /* decode append with len == capacity */
+  RECO_DEV_BAD_RETENTION = 2,    /* retention r not in (0, 1] (or NaN) */
+  RECO_DEV_BAD_SCORE = 3,        /* NaN or negative importance score */
+  RECO_DEV_BAD_TOKEN_ID = 4,     /* reflection id or answer token outside [0, vocab) */
+  RECO_DEV_BAD_LENGTH = 5        /* stored len outside [0, capacity] */
+};
+
+/* reco_score flags */
+enum { RECO_SCORE_CAUSAL = 1u };  /* window query at position p sees keys 0..p only */
+
+/* [host] description of a KV cache; read during the call, not retained. */
+typedef struct reco_kv_cache {
+  void *k;              /* [n_layers][batch][n_kv_heads][capacity][head_dim] */
+  void *v;              /* same layout as k */
+  int32_t *len;         /* [n_layers][batch][n_kv_heads], valid rows per unit (in/out) */
+  int32_t n_layers;     /* layers held by the cache (>= 1) */
+  int32_t batch;        /* sequences (>= 1) */
+  int32_t n_kv_heads;   /* KV heads per layer (>= 1) */
+  int32_t capacity;     /* rows per unit (>= 1) */
+  int32_t head_dim;     /* 64 or 128 */
+  int32_t dtype;        /* reco_dtype_t; every cache-typed tensor uses it */
+} reco_kv_cache_t;
+
+/* ------------------------------------------------------------------------ */
+/* Eq. 2 (Section 3.2, attention-guided selection): importance of every cached
+ * key as the attention mass it receives from the w most recent tokens.
+ * For every unit (layer, sequence, kv head h) with L = len[unit] and
+ * w_eff = min(w, L), the window query of position p = L - w + t (row t of
+ * q_win, rows with p < 0 are ignored) of each query head in h's group gives a
+ * softmax over keys 0..L-1 (0..p when RECO_SCORE_CAUSAL is set) of
+ * scale * <q, k_j>; scores[unit][j] is the sum of these softmax rows over the
+ * window and the group, for every j < L.  Entries j >= L are left untouched.
+ *   q_win : [n_layers][batch][n_q_heads][w][head_dim], cache dtype
+ *   scale : logit scale, normally 1/sqrt(head_dim)
+ *   scores: [n_layers][batch][n_kv_heads][capacity] fp32 (output)
+ * Requires 1 <= w <= capacity and G * w <= 4096.  Accumulation is fp32. */
+size_t reco_score_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers,
+                                 int32_t n_q_heads, int32_t w);
+reco_status_t reco_score(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,
+                         const void *q_win, int32_t n_q_heads, int32_t w, float scale,
+                         uint32_t flags, float *scores, void *ws, size_t ws_bytes,
+                         int32_t *dev_err, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Section 3.2 (reward-driven retention and attention-guided selection):
+ * per unit with L = len[unit], w_eff = min(w, L) and r = retention[seq],
+ *   m = min(L, max(w_eff, ceil(r * L)))      (r * L as an IEEE fp64 product)
+ * rows are kept: the window [L - w_eff, L) and the k = m - w_eff prefix
+ * positions with the largest scores[unit][j] (ties: lower j first).  The kept
+ * rows of K and V are moved, in ascending order, to rows 0..m-1 of the same
+ * unit (bit-exact copies; rows >= m keep unspecified contents) and len is set
+ * to m.
+ *   scores    : [n_layers][batch][n_kv_heads][capacity] fp32, >= 0 (from reco_score)
+ *   retention : [batch] fp64 in (0, 1]
+ *   kept_idx  : nullable [n_layers][batch][n_kv_heads][capacity] int32 output;
+ *               the first m entries of each unit receive the kept positions
+ *               (ascending, in pre-compaction numbering)
+ * A unit whose r or scores are invalid is left unchanged and dev_err is set. */
+size_t reco_select_compact_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers);
+reco_status_t reco_select_compact(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,
+                                  const float *scores, const double *retention, int32_t w,
+                                  int32_t *kept_idx, void *ws, size_t ws_bytes,
+                                  int32_t *dev_err, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Decode attention over the retained cache (the per-token attention cost of
+ * Section 1 that compression reduces).  For every query head hq of every
+ * covered (layer, sequence), with h = hq / G and n = len[unit of h]:
+ *   if k_new != NULL the new token's row (k_new, v_new) takes part as key n
+ *   (it attends to itself) and, after the attention, is written to row n of
+ *   the cache and len is incremented;
+ *   out[hq] = sum_j softmax_j(scale * <q[hq], k_j>) v_j over the keys j,
+ *   lse[hq] = natural log-sum-exp of the scaled logits.
+ * With no keys at all out is 0 and lse is -inf.
+ *   q            : [n_layers][batch][n_q_heads][head_dim], cache dtype
+ *   k_new, v_new : both NULL (no append) or [n_layers][batch][n_kv_heads][head_dim]
+ *   out          : [n_layers][batch][n_q_heads][head_dim], cache dtype (output)
+ *   lse          : nullable [n_layers][batch][n_q_heads] fp32 (output)
+ * An append with len == capacity is not performed (the token still takes part
+ * in the attention) and sets RECO_DEV_APPEND_OVERFLOW. */
+size_t reco_decode_attn_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers,
+                                       int32_t n_q_heads);
+reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,
+                               const void *q, int32_t n_q_heads, float scale,
+                               const void *k_new, const void *v_new, void *out, float *lse,
+                               void *ws, size_t ws_bytes, int32_t *dev_err, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Eq. 3 and Eq. 4 (Section 3.3, reward-banded reflection penalty): for every
+ * row b, beta_b = beta_lo if reward[b] <= tau_lo, beta_hi if
+ * reward[b] >= tau_hi, beta_mid otherwise (fp32 comparisons), and
+ * logits[b][u] -= beta_b (one fp32 subtraction) for every DISTINCT id u in
+ * refl_ids.  All other logits are untouched (bit-exact).
+ *   logits   : [rows][ld] fp32, in place; ld >= vocab
+ *   refl_ids : [n_refl] int32, 0 <= n_refl <= 4096, each in [0, vocab)
+ *   reward   : [rows] fp32
+ * An id outside [0, vocab) is skipped and sets RECO_DEV_BAD_TOKEN_ID. */
+reco_status_t reco_logit_penalty(float *logits, int32_t rows, int32_t vocab, int64_t ld,
+                                 const int32_t *refl_ids, int32_t n_refl, const float *reward,
+                                 float tau_lo, float tau_hi, float beta_lo, float beta_mid,
+                                 float beta_hi, int32_t *dev_err, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Eq. 5 and Eq. 6 (Section 3.3, early stopping via answer confidence): for
+ * every sequence b, ppl[b] = exp((1/n) sum_t (LSE(logits[b][t]) -
+ * logits[b][t][tokens[b][t]])) with natural logarithms, and
+ * stop[b] = (ppl[b] <= tau_p).
+ *   logits : [batch][n][vocab] fp32 (the probe answer's raw logits)
+ *   tokens : [batch][n] int32 in [0, vocab)
+ *   ppl    : [batch] fp32 (output);  stop : nullable [batch] int32 (output)
+ * Row log-sum-exps are fp32 partials merged in fp64.  A token out of range
+ * makes ppl NaN for its sequence and sets RECO_DEV_BAD_TOKEN_ID. */
+size_t reco_answer_ppl_workspace_size(int32_t batch, int32_t n, int32_t vocab);
+reco_status_t reco_answer_ppl(const float *logits, const int32_t *tokens, int32_t batch,
+                              int32_t n, int32_t vocab, float tau_p, float *ppl, int32_t *stop,
+                              void *ws, size_t ws_bytes, int32_t *dev_err, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* [host] Reward -> retention policies (Section 3.2).  Pure functions.
+ * reco_retention_from_reward: r = clamp(1 - v/2, lo, hi) in fp64.
+ * reco_retention_eq1: Eq. 1, lambda_i = lambda - delta * (v_i - mean) /
+ *   (max - min) over v_hist[0..n) (latest last, included); lambda when all
+ *   rewards are equal; NaN when n < 1 or v_hist is NULL. */
+double reco_retention_from_reward(double v, double lo, double hi);
+double reco_retention_eq1(const double *v_hist, int32_t n, double lambda, double delta);
+
+/* [host] Human-readable status and the ABI version (RECO_ABI_VERSION). */
+const char *reco_status_str(reco_status_t status);
+int32_t reco_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RECO_H */

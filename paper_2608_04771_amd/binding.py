@@ -1,0 +1,277 @@
+"""Thin Python binding of libreco.so (argument marshalling only).
+
+Each function has the name of the C entry point it calls and forwards device
+pointers (``tensor.data_ptr()``) and the current HIP stream of torch.  Every
+step of the computation runs in the HIP kernels of the library; nothing here
+computes a result.  The library must have been built in-tree
+(``python -m paper_2608_04771_amd.build``); importing it otherwise fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libreco.so")
+
+RECO_OK = 0
+RECO_ERR_INVALID_ARG = 1
+RECO_ERR_UNSUPPORTED = 2
+RECO_ERR_WORKSPACE = 3
+RECO_ERR_HIP = 4
+RECO_F32 = 0
+RECO_BF16 = 1
+RECO_SCORE_CAUSAL = 1
+DEV_ERRORS = {0: "ok", 1: "append overflow", 2: "bad retention", 3: "bad score", 4: "bad token id",
+              5: "bad length"}
+
+EXPORTED = [
+    "reco_score_workspace_size", "reco_score", "reco_select_compact_workspace_size", "reco_select_compact",
+    "reco_decode_attn_workspace_size", "reco_decode_attn", "reco_logit_penalty",
+    "reco_answer_ppl_workspace_size", "reco_answer_ppl", "reco_retention_from_reward", "reco_retention_eq1",
+    "reco_status_str", "reco_abi_version",
+]
+
+
+class RecoKVCache(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("len", ctypes.c_void_p),
+                ("n_layers", ctypes.c_int32), ("batch", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("capacity", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libreco.so; raises if it has not been built (no fallback exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"HIP library missing: {path} (build it with `python -m paper_2608_04771_amd.build`)")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, F32, F64, SZ, U32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                      ctypes.c_double, ctypes.c_size_t, ctypes.c_uint32)
+    C = ctypes.POINTER(RecoKVCache)
+    sig = {
+        "reco_score_workspace_size": (SZ, [C, I32, I32, I32]),
+        "reco_score": (I32, [C, I32, I32, P, I32, I32, F32, U32, P, P, SZ, P, P]),
+        "reco_select_compact_workspace_size": (SZ, [C, I32]),
+        "reco_select_compact": (I32, [C, I32, I32, P, P, I32, P, P, SZ, P, P]),
+        "reco_decode_attn_workspace_size": (SZ, [C, I32, I32]),
+        "reco_decode_attn": (I32, [C, I32, I32, P, I32, F32, P, P, P, P, P, SZ, P, P]),
+        "reco_logit_penalty": (I32, [P, I32, I32, I64, P, I32, P, F32, F32, F32, F32, F32, P, P]),
+        "reco_answer_ppl_workspace_size": (SZ, [I32, I32, I32]),
+        "reco_answer_ppl": (I32, [P, P, I32, I32, I32, F32, P, P, P, SZ, P, P]),
+        "reco_retention_from_reward": (F64, [F64, F64, F64]),
+        "reco_retention_eq1": (F64, [ctypes.POINTER(ctypes.c_double), I32, F64, F64]),
+        "reco_status_str": (ctypes.c_char_p, [I32]),
+        "reco_abi_version": (I32, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check(status: int, what: str):
+    if status != RECO_OK:
+        msg = load_library().reco_status_str(status).decode()
+        raise RuntimeError(f"{what} failed: {msg} (status {status})")
+
+
+def _need_cuda(*ts):
+    for t in ts:
+        if t is not None:
+            if not t.is_cuda:
+                raise ValueError("tensors must live on the GPU")
+            if not t.is_contiguous():
+                raise ValueError("tensors must be contiguous")
+
+
+class KVCache:
+    """A KV cache in the library's layout: K and V ``[NL][B][H][Cap][D]``
+    (fp32 or bf16), ``length`` ``[NL][B][H]`` int32, all on the GPU."""
+
+    def __init__(self, k: torch.Tensor, v: torch.Tensor, length: torch.Tensor):
+        _need_cuda(k, v, length)
+        if k.shape != v.shape or k.dim() != 5 or k.dtype != v.dtype:
+            raise ValueError("k and v must share a [NL][B][H][Cap][D] shape and dtype")
+        if k.dtype not in (torch.float32, torch.bfloat16):
+            raise ValueError("cache dtype must be float32 or bfloat16")
+        if length.dtype != torch.int32 or tuple(length.shape) != tuple(k.shape[:3]):
+            raise ValueError("length must be int32 [NL][B][H]")
+        self.k, self.v, self.length = k, v, length
+        NL, B, H, Cap, D = k.shape
+        self.struct = RecoKVCache(k.data_ptr(), v.data_ptr(), length.data_ptr(), NL, B, H, Cap, D,
+                                  RECO_F32 if k.dtype == torch.float32 else RECO_BF16)
+
+    @property
+    def shape(self):
+        return tuple(self.k.shape)
+
+    def ref(self):
+        return ctypes.byref(self.struct)
+
+
+def _layers(cache: KVCache, layer0: int, n_layers: Optional[int]):
+    return layer0, (cache.shape[0] - layer0) if n_layers is None else n_layers
+
+
+def score_workspace_size(cache: KVCache, n_q_heads: int, w: int, n_layers: Optional[int] = None) -> int:
+    nl = cache.shape[0] if n_layers is None else n_layers
+    return int(load_library().reco_score_workspace_size(cache.ref(), nl, n_q_heads, w))
+
+
+def select_compact_workspace_size(cache: KVCache, n_layers: Optional[int] = None) -> int:
+    nl = cache.shape[0] if n_layers is None else n_layers
+    return int(load_library().reco_select_compact_workspace_size(cache.ref(), nl))
+
+
+def decode_attn_workspace_size(cache: KVCache, n_q_heads: int, n_layers: Optional[int] = None) -> int:
+    nl = cache.shape[0] if n_layers is None else n_layers
+    return int(load_library().reco_decode_attn_workspace_size(cache.ref(), nl, n_q_heads))
+
+
+def answer_ppl_workspace_size(batch: int, n: int, vocab: int) -> int:
+    return int(load_library().reco_answer_ppl_workspace_size(batch, n, vocab))
+
+
+def _ws(nbytes: int, device, ws: Optional[torch.Tensor]) -> torch.Tensor:
+    if ws is not None:
+        return ws
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[float] = None, causal: bool = True,
+               scores: Optional[torch.Tensor] = None, layer0: int = 0, n_layers: Optional[int] = None,
+               ws: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Eq. 2 window attention mass; returns scores [NL][B][H][Cap] fp32."""
+    layer0, nl = _layers(cache, layer0, n_layers)
+    NL, B, H, Cap, D = cache.shape
+    if q_win.dim() != 5 or q_win.shape[0] != nl or q_win.shape[1] != B or q_win.shape[3] != w or q_win.shape[4] != D:
+        raise ValueError("q_win must be [n_layers][B][Hq][w][D]")
+    if q_win.dtype != cache.k.dtype:
+        raise ValueError("q_win must have the cache dtype")
+    hq = q_win.shape[2]
+    if scores is None:
+        scores = torch.zeros((nl, B, H, Cap), dtype=torch.float32, device=cache.k.device)
+    _need_cuda(q_win, scores, ws, dev_err)
+    ws = _ws(score_workspace_size(cache, hq, w, nl), cache.k.device, ws)
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    st = load_library().reco_score(cache.ref(), layer0, nl, _ptr(q_win), hq, w, scale,
+                                   RECO_SCORE_CAUSAL if causal else 0, _ptr(scores), _ptr(ws), ws.numel(),
+                                   _ptr(dev_err), _stream(cache.k.device))
+    _check(st, "reco_score")
+    return scores
+
+
+def reco_select_compact(cache: KVCache, scores: torch.Tensor, retention: torch.Tensor, w: int,
+                        kept_idx: Optional[torch.Tensor] = None, layer0: int = 0, n_layers: Optional[int] = None,
+                        ws: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None):
+    """Select the reward budget per unit and compact K/V in place (len <- m)."""
+    layer0, nl = _layers(cache, layer0, n_layers)
+    if retention.dtype != torch.float64 or retention.numel() != cache.shape[1]:
+        raise ValueError("retention must be float64 [B]")
+    if scores.dtype != torch.float32:
+        raise ValueError("scores must be float32")
+    if kept_idx is not None and kept_idx.dtype != torch.int32:
+        raise ValueError("kept_idx must be int32")
+    _need_cuda(scores, retention, kept_idx, ws, dev_err)
+    ws = _ws(select_compact_workspace_size(cache, nl), cache.k.device, ws)
+    st = load_library().reco_select_compact(cache.ref(), layer0, nl, _ptr(scores), _ptr(retention), w,
+                                            _ptr(kept_idx), _ptr(ws), ws.numel(), _ptr(dev_err),
+                                            _stream(cache.k.device))
+    _check(st, "reco_select_compact")
+    return kept_idx
+
+
+def reco_decode_attn(cache: KVCache, q: torch.Tensor, k_new: Optional[torch.Tensor] = None,
+                     v_new: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+                     out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None, want_lse: bool = True,
+                     layer0: int = 0, n_layers: Optional[int] = None, ws: Optional[torch.Tensor] = None,
+                     dev_err: Optional[torch.Tensor] = None):
+    """GQA decode attention (optionally appending the new token); returns (out, lse)."""
+    layer0, nl = _layers(cache, layer0, n_layers)
+    NL, B, H, Cap, D = cache.shape
+    if q.dim() != 4 or q.shape[0] != nl or q.shape[1] != B or q.shape[3] != D or q.dtype != cache.k.dtype:
+        raise ValueError("q must be [n_layers][B][Hq][D] in the cache dtype")
+    hq = q.shape[2]
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((nl, B, hq), dtype=torch.float32, device=q.device)
+    _need_cuda(q, k_new, v_new, out, lse, ws, dev_err)
+    ws = _ws(decode_attn_workspace_size(cache, hq, nl), q.device, ws)
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    st = load_library().reco_decode_attn(cache.ref(), layer0, nl, _ptr(q), hq, scale, _ptr(k_new), _ptr(v_new),
+                                         _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _ptr(dev_err),
+                                         _stream(q.device))
+    _check(st, "reco_decode_attn")
+    return out, lse
+
+
+def reco_logit_penalty(logits: torch.Tensor, refl_ids: torch.Tensor, reward: torch.Tensor, tau_lo: float,
+                       tau_hi: float, beta_lo: float, beta_mid: float, beta_hi: float,
+                       dev_err: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Eq. 3-4 in place on fp32 logits [rows][vocab] (row stride may exceed vocab)."""
+    if logits.dtype != torch.float32 or logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be fp32 [rows][vocab] with unit column stride")
+    if refl_ids.dtype != torch.int32 or reward.dtype != torch.float32:
+        raise ValueError("refl_ids int32, reward float32")
+    for t in (refl_ids, reward, dev_err):
+        _need_cuda(t)
+    if not logits.is_cuda:
+        raise ValueError("logits must live on the GPU")
+    rows, vocab = logits.shape
+    st = load_library().reco_logit_penalty(_ptr(logits), rows, vocab, logits.stride(0), _ptr(refl_ids),
+                                           refl_ids.numel(), _ptr(reward), tau_lo, tau_hi, beta_lo, beta_mid,
+                                           beta_hi, _ptr(dev_err), _stream(logits.device))
+    _check(st, "reco_logit_penalty")
+    return logits
+
+
+def reco_answer_ppl(logits: torch.Tensor, tokens: torch.Tensor, tau_p: float, ppl: Optional[torch.Tensor] = None,
+                    stop: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                    dev_err: Optional[torch.Tensor] = None):
+    """Eq. 5-6: returns (ppl [B] fp32, stop [B] int32)."""
+    if logits.dtype != torch.float32 or logits.dim() != 3 or tokens.dtype != torch.int32:
+        raise ValueError("logits fp32 [B][n][V], tokens int32 [B][n]")
+    B, n, V = logits.shape
+    if ppl is None:
+        ppl = torch.empty(B, dtype=torch.float32, device=logits.device)
+    if stop is None:
+        stop = torch.empty(B, dtype=torch.int32, device=logits.device)
+    _need_cuda(logits, tokens, ppl, stop, ws, dev_err)
+    ws = _ws(answer_ppl_workspace_size(B, n, V), logits.device, ws)
+    st = load_library().reco_answer_ppl(_ptr(logits), _ptr(tokens), B, n, V, tau_p, _ptr(ppl), _ptr(stop),
+                                        _ptr(ws), ws.numel(), _ptr(dev_err), _stream(logits.device))
+    _check(st, "reco_answer_ppl")
+    return ppl, stop
+
+
+def reco_retention_from_reward(v: float, lo: float = 0.3, hi: float = 1.0) -> float:
+    return float(load_library().reco_retention_from_reward(float(v), float(lo), float(hi)))
+
+
+def reco_retention_eq1(v_hist: Sequence[float], lam: float = 0.25, delta: float = 0.1) -> float:
+    arr = (ctypes.c_double * len(v_hist))(*[float(x) for x in v_hist])
+    return float(load_library().reco_retention_eq1(arr, len(v_hist), float(lam), float(delta)))
+
+
+def reco_abi_version() -> int:
+    return int(load_library().reco_abi_version())

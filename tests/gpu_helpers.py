@@ -1,0 +1,81 @@
+"""Shared helpers of the GPU parity tests: upload seeded inputs, bring device
+results back as exact float64 arrays, and the comparison rules.
+
+Tolerances (written here once, used by every GPU test):
+* decode output, fp32 caches: |gpu - oracle| <= 1e-5 * max(1, max_d |oracle row|);
+* decode output, bf16 caches: |gpu - oracle| <= 2e-2 (fp32 accumulation, bf16 output);
+* decode log-sum-exp: 1e-5 absolute (fp32) and 1e-4 absolute (bf16 inputs);
+* scores: relative error <= SCORE_RTOL (a diagnostic bound; the kept-index
+  check below is the contract);
+* kept indices: equal sets except positions whose oracle score lies within
+  1e-6 relative of the oracle's k-th prefix score (ties);
+* gathered K/V rows and appended rows: bit-exact.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2608_04771_amd import binding as B
+from paper_2608_04771_amd import inputs as I
+
+SCORE_RTOL = 2e-6
+TIE_RTOL = 1e-6
+
+
+def f64(t: torch.Tensor) -> np.ndarray:
+    return I.to_f64(t)
+
+
+def upload(ci: I.CacheInputs, device="cuda"):
+    k = ci.k.to(device).contiguous()
+    v = ci.v.to(device).contiguous()
+    ln = ci.length.to(device).contiguous()
+    return B.KVCache(k, v, ln)
+
+
+def assert_decode_close(gpu_out: torch.Tensor, ref: np.ndarray, dtype: str, what: str = ""):
+    g = f64(gpu_out)
+    if dtype == "f32":
+        scale = np.maximum(1.0, np.abs(ref).max(axis=-1, keepdims=True))
+        err = np.abs(g - ref) / scale
+        assert err.max() <= 1e-5, f"{what}: fp32 decode rel err {err.max():.3e}"
+    else:
+        err = np.abs(g - ref)
+        assert err.max() <= 2e-2, f"{what}: bf16 decode abs err {err.max():.3e}"
+    return float(err.max())
+
+
+def assert_lse_close(gpu_lse: torch.Tensor, ref: np.ndarray, dtype: str, what: str = ""):
+    g = f64(gpu_lse)
+    tol = 1e-5 if dtype == "f32" else 1e-4
+    fin = np.isfinite(ref)
+    assert (np.isfinite(g) == fin).all(), f"{what}: lse finiteness differs"
+    err = np.abs(g[fin] - ref[fin]).max() if fin.any() else 0.0
+    assert err <= tol, f"{what}: lse err {err:.3e}"
+    return float(err)
+
+
+def kept_sets_match(idx_gpu: np.ndarray, s_or: np.ndarray, L: int, w: int, r: float):
+    """Compare a GPU kept list with the oracle's selection, excusing ties at the
+    k-th value.  Returns (ok, message)."""
+    ref = oracle.select_unit(s_or, L, w, r)
+    m = len(ref)
+    g = np.asarray(idx_gpu[:m], dtype=np.int64)
+    if len(g) != m or not (np.diff(g) > 0).all():
+        return False, "gpu list not strictly increasing / wrong length"
+    w_eff = min(w, L)
+    P = L - w_eff
+    if not (g[m - w_eff:] == np.arange(P, L)).all():
+        return False, "window not kept in place"
+    kg, kr = set(g[:m - w_eff].tolist()), set(ref[:m - w_eff].tolist())
+    diff = kg ^ kr
+    if not diff:
+        return True, "exact"
+    k = m - w_eff
+    theta = np.sort(s_or[:P])[::-1][k - 1]
+    bad = [j for j in diff if abs(s_or[j] - theta) > TIE_RTOL * theta]
+    if bad:
+        return False, f"unexcused swaps {bad[:5]} theta={theta} scores={[s_or[j] for j in bad[:5]]}"
+    return True, f"{len(diff)} excused tie swaps"

@@ -1,0 +1,152 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every entry point the header declares, and rejects invalid arguments before
+launching anything.  Validation precedes every HIP call, so these calls are
+safe on a machine without a GPU."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_04771_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "reco.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^[A-Za-z][A-Za-z0-9_ ]*[ *]+(reco_\w+)\(", text, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.load_library()
+    names = _declared()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(B.EXPORTED)
+
+
+def test_abi_version_and_status_strings():
+    lib = B.load_library()
+    assert B.reco_abi_version() == 1
+    assert lib.reco_status_str(0) == b"ok"
+    assert b"workspace" in lib.reco_status_str(3)
+    assert lib.reco_status_str(99) == b"unknown status"
+
+
+def test_retention_policies_match_oracle():
+    for v in np.linspace(0, 1, 41):
+        assert B.reco_retention_from_reward(v) == oracle.retention_from_reward(v)
+    rng = np.random.default_rng(0)
+    for _ in range(100):
+        hist = rng.uniform(0, 1, size=rng.integers(1, 20))
+        assert B.reco_retention_eq1(hist, 0.25, 0.1) == pytest.approx(oracle.retention_eq1(hist, 0.25, 0.1),
+                                                                         rel=0, abs=1e-15)
+    assert B.reco_retention_eq1([0.4, 0.4], 0.25, 0.1) == 0.25
+
+
+def _fake_cache(**kw):
+    d = dict(k=0x1000, v=0x2000, len=0x3000, n_layers=2, batch=1, n_kv_heads=2, capacity=64, head_dim=128,
+             dtype=B.RECO_BF16)
+    d.update(kw)
+    return B.RecoKVCache(d["k"], d["v"], d["len"], d["n_layers"], d["batch"], d["n_kv_heads"], d["capacity"],
+                         d["head_dim"], d["dtype"])
+
+
+P = ctypes.c_void_p
+
+
+def _score(c, layer0=0, nl=2, q=0x10, hq=4, w=8, scale=0.1, flags=1, scores=0x20, ws=0x30, wsb=1 << 30):
+    lib = B.load_library()
+    return lib.reco_score(ctypes.byref(c), layer0, nl, P(q), hq, w, scale, flags, P(scores), P(ws), wsb, None, None)
+
+
+def test_score_rejects_bad_arguments():
+    ok = _fake_cache()
+    assert _score(_fake_cache(k=0)) == B.RECO_ERR_INVALID_ARG
+    assert _score(ok, q=0) == B.RECO_ERR_INVALID_ARG
+    assert _score(ok, scores=0) == B.RECO_ERR_INVALID_ARG
+    assert _score(ok, layer0=1, nl=2) == B.RECO_ERR_INVALID_ARG          # past the last layer
+    assert _score(ok, nl=0) == B.RECO_ERR_INVALID_ARG
+    assert _score(ok, hq=3) == B.RECO_ERR_INVALID_ARG                    # not a multiple of n_kv_heads
+    assert _score(ok, w=0) == B.RECO_ERR_INVALID_ARG
+    assert _score(ok, w=65) == B.RECO_ERR_INVALID_ARG                    # window beyond capacity
+    assert _score(ok, scale=float("nan")) == B.RECO_ERR_INVALID_ARG
+    assert _score(ok, flags=2) == B.RECO_ERR_INVALID_ARG
+    assert _score(_fake_cache(head_dim=96)) == B.RECO_ERR_UNSUPPORTED
+    assert _score(_fake_cache(dtype=7)) == B.RECO_ERR_UNSUPPORTED
+    assert _score(ok, ws=0) == B.RECO_ERR_WORKSPACE
+    assert _score(ok, wsb=16) == B.RECO_ERR_WORKSPACE
+    big = _fake_cache(capacity=100000)
+    assert _score(big, hq=2 * 100, w=100) == B.RECO_ERR_UNSUPPORTED      # G*w = 10000 rows > 4096
+
+
+def test_select_compact_rejects_bad_arguments():
+    lib = B.load_library()
+    c = _fake_cache()
+
+    def call(cache=c, scores=0x20, ret=0x40, w=8, idx=None, ws=0x30, wsb=1 << 30, layer0=0, nl=2):
+        return lib.reco_select_compact(ctypes.byref(cache), layer0, nl, P(scores), P(ret), w, P(idx) if idx else None,
+                                       P(ws), wsb, None, None)
+    assert call(scores=0) == B.RECO_ERR_INVALID_ARG
+    assert call(ret=0) == B.RECO_ERR_INVALID_ARG
+    assert call(w=0) == B.RECO_ERR_INVALID_ARG
+    assert call(w=65) == B.RECO_ERR_INVALID_ARG
+    assert call(layer0=-1) == B.RECO_ERR_INVALID_ARG
+    assert call(cache=_fake_cache(head_dim=32)) == B.RECO_ERR_UNSUPPORTED
+    assert call(ws=0) == B.RECO_ERR_WORKSPACE
+    need = lib.reco_select_compact_workspace_size(ctypes.byref(c), 2)
+    assert need > 0
+    assert call(wsb=need - 1) == B.RECO_ERR_WORKSPACE
+
+
+def test_decode_rejects_bad_arguments():
+    lib = B.load_library()
+    c = _fake_cache()
+
+    def call(cache=c, q=0x10, hq=4, scale=0.1, kn=None, vn=None, out=0x50, ws=0x30, wsb=1 << 30):
+        return lib.reco_decode_attn(ctypes.byref(cache), 0, 2, P(q), hq, scale, P(kn) if kn else None,
+                                    P(vn) if vn else None, P(out), None, P(ws), wsb, None, None)
+    assert call(q=0) == B.RECO_ERR_INVALID_ARG
+    assert call(out=0) == B.RECO_ERR_INVALID_ARG
+    assert call(kn=0x60) == B.RECO_ERR_INVALID_ARG                        # k_new without v_new
+    assert call(hq=5) == B.RECO_ERR_INVALID_ARG
+    assert call(scale=float("inf")) == B.RECO_ERR_INVALID_ARG
+    assert call(hq=2 * 17) == B.RECO_ERR_UNSUPPORTED                      # G = 17 > 16
+    assert call(ws=0) == B.RECO_ERR_WORKSPACE
+    assert call(wsb=8) == B.RECO_ERR_WORKSPACE
+
+
+def test_penalty_and_ppl_reject_bad_arguments():
+    lib = B.load_library()
+    pen = lambda logits=0x10, rows=1, vocab=100, ld=100, ids=0x20, n=4, rew=0x30: lib.reco_logit_penalty(  # noqa: E731
+        P(logits), rows, vocab, ld, P(ids), n, P(rew), 0.4, 0.8, 0.0, 1.0, 3.0, None, None)
+    assert pen(logits=0) == B.RECO_ERR_INVALID_ARG
+    assert pen(ld=99) == B.RECO_ERR_INVALID_ARG
+    assert pen(n=-1) == B.RECO_ERR_INVALID_ARG
+    assert pen(n=5000) == B.RECO_ERR_INVALID_ARG
+    assert pen(rew=0) == B.RECO_ERR_INVALID_ARG
+    assert pen(n=0, ids=0) == B.RECO_OK                                   # empty set: nothing to do
+    ppl = lambda logits=0x10, tok=0x20, b=2, n=4, v=100, out=0x30, ws=0x40, wsb=1 << 20: lib.reco_answer_ppl(  # noqa: E731
+        P(logits), P(tok), b, n, v, 1.1, P(out), None, P(ws), wsb, None, None)
+    assert ppl(logits=0) == B.RECO_ERR_INVALID_ARG
+    assert ppl(n=0) == B.RECO_ERR_INVALID_ARG
+    assert ppl(out=0) == B.RECO_ERR_INVALID_ARG
+    assert ppl(ws=0) == B.RECO_ERR_WORKSPACE
+    assert ppl(wsb=4) == B.RECO_ERR_WORKSPACE
+
+
+def test_workspace_sizes_are_positive_and_monotone():
+    lib = B.load_library()
+    small, big = _fake_cache(capacity=64), _fake_cache(capacity=4096)
+    for fn, args in [("reco_score_workspace_size", (2, 4, 8)), ("reco_decode_attn_workspace_size", (2, 4)),
+                     ("reco_select_compact_workspace_size", (2,))]:
+        a = getattr(lib, fn)(ctypes.byref(small), *args)
+        b = getattr(lib, fn)(ctypes.byref(big), *args)
+        assert 0 < a <= b, fn
+    assert lib.reco_answer_ppl_workspace_size(8, 32, 152064) >= 8 * 32 * 2 * 4
+    assert lib.reco_answer_ppl_workspace_size(0, 32, 10) == 0

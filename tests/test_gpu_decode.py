@@ -1,0 +1,108 @@
+"""GPU parity of reco_decode_attn against the CPU oracle (decode_cache)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import assert_decode_close, assert_lse_close, f64, upload
+from paper_2608_04771_amd import binding as B
+from paper_2608_04771_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def _random_cache(NL, Bsz, H, Cap, D, dtype, lens, seed):
+    g = torch.Generator().manual_seed(seed)
+    td = torch.float32 if dtype == "f32" else torch.bfloat16
+    k = torch.randn((NL, Bsz, H, Cap, D), generator=g).to(td)
+    v = torch.randn((NL, Bsz, H, Cap, D), generator=g).to(td)
+    ln = torch.tensor(lens, dtype=torch.int32).reshape(NL, Bsz, H)
+    return k, v, ln
+
+
+@pytest.mark.parametrize("dtype,D,G", [("f32", 64, 4), ("f32", 128, 7), ("bf16", 128, 7), ("bf16", 64, 4),
+                                       ("bf16", 128, 1), ("bf16", 128, 16), ("f32", 64, 5), ("bf16", 128, 8)])
+@pytest.mark.parametrize("append", [False, True])
+def test_decode_ragged_units(dtype, D, G, append):
+    """Ragged per-unit lengths spanning empty, single-row, tile edges and a
+    nearly full unit; every query head compared with the oracle."""
+    NL, Bsz, H, Cap = 2, 2, 3, 1100
+    lens = [0, 1, 31, 32, 33, 64, 65, 1000, 1099, 517, 250, 7]
+    if not append:
+        lens[0] = 3                                        # attention over nothing is undefined
+    k, v, ln = _random_cache(NL, Bsz, H, Cap, D, dtype, lens, seed=D * 100 + G * 3 + (dtype == "f32"))
+    td = k.dtype
+    gq = torch.Generator().manual_seed(5)
+    q = torch.randn((NL, Bsz, H * G, D), generator=gq).to(td)
+    kn = torch.randn((NL, Bsz, H, D), generator=gq).to(td) if append else None
+    vn = torch.randn((NL, Bsz, H, D), generator=gq).to(td) if append else None
+    cache = B.KVCache(k.cuda(), v.cuda(), ln.cuda())
+    dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out, lse = B.reco_decode_attn(cache, q.cuda(), None if kn is None else kn.cuda(),
+                                  None if vn is None else vn.cuda(), dev_err=dev_err)
+    torch.cuda.synchronize()
+    K, V, lens_np = f64(k), f64(v), ln.numpy().astype(np.int64).copy()
+    ref_out, ref_lse = oracle.decode_cache(K, V, lens_np, f64(q), 1 / np.sqrt(D),
+                                           None if kn is None else f64(kn), None if vn is None else f64(vn))
+    assert dev_err.item() == 0
+    assert_decode_close(out, ref_out, dtype, f"{dtype} D={D} G={G}")
+    assert_lse_close(lse, ref_lse, dtype, f"{dtype} D={D} G={G}")
+    if append:
+        assert (cache.length.cpu().numpy() == lens_np).all()
+        kc, vc = cache.k.cpu(), cache.v.cpu()
+        for idx in np.ndindex(NL, Bsz, H):
+            n = int(ln[idx])
+            assert torch.equal(kc[idx][n], kn[idx]) and torch.equal(vc[idx][n], vn[idx])
+            assert torch.equal(kc[idx][:n], k[idx][:n])
+
+
+def test_decode_append_overflow_is_reported():
+    NL, Bsz, H, Cap, D, G = 1, 1, 2, 64, 128, 4
+    k, v, ln = _random_cache(NL, Bsz, H, Cap, D, "bf16", [64, 10], seed=3)
+    q = torch.randn((NL, Bsz, H * G, D)).to(torch.bfloat16)
+    kn = torch.randn((NL, Bsz, H, D)).to(torch.bfloat16)
+    vn = torch.randn((NL, Bsz, H, D)).to(torch.bfloat16)
+    cache = B.KVCache(k.cuda(), v.cuda(), ln.cuda())
+    dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out, _ = B.reco_decode_attn(cache, q.cuda(), kn.cuda(), vn.cuda(), dev_err=dev_err)
+    torch.cuda.synchronize()
+    assert dev_err.item() == 1
+    assert cache.length.cpu().tolist() == [[[64, 11]]]
+    # the full unit still attends over its 64 rows plus the new token
+    ref, _ = oracle.decode_unit(f64(k)[0, 0, 0], f64(v)[0, 0, 0], 64, f64(q)[0, 0, :G], 1 / np.sqrt(D),
+                                f64(kn)[0, 0, 0], f64(vn)[0, 0, 0])
+    assert np.abs(f64(out)[0, 0, :G] - ref).max() <= 2e-2
+
+
+def test_decode_layer_range_touches_only_its_layers():
+    NL, Bsz, H, Cap, D, G = 4, 1, 2, 300, 128, 7
+    k, v, ln = _random_cache(NL, Bsz, H, Cap, D, "bf16", [200, 150] * 4, seed=4)
+    cache = B.KVCache(k.cuda(), v.cuda(), ln.cuda())
+    q = torch.randn((2, Bsz, H * G, D)).to(torch.bfloat16)
+    kn = torch.randn((2, Bsz, H, D)).to(torch.bfloat16)
+    vn = torch.randn((2, Bsz, H, D)).to(torch.bfloat16)
+    out, lse = B.reco_decode_attn(cache, q.cuda(), kn.cuda(), vn.cuda(), layer0=1, n_layers=2)
+    torch.cuda.synchronize()
+    K, V, L = f64(k)[1:3].copy(), f64(v)[1:3].copy(), ln.numpy()[1:3].astype(np.int64).copy()
+    ref, rl = oracle.decode_cache(K, V, L, f64(q), 1 / np.sqrt(D), f64(kn), f64(vn))
+    assert_decode_close(out, ref, "bf16")
+    assert_lse_close(lse, rl, "bf16")
+    assert cache.length.cpu().numpy().reshape(-1).tolist() == [200, 150, 201, 151, 201, 151, 200, 150]
+    assert torch.equal(cache.k.cpu()[0], k[0]) and torch.equal(cache.k.cpu()[3], k[3])
+
+
+def test_decode_tiny_workload_64_steps():
+    """The tiny fp32 workload: uncompressed cache, 64 decode steps with append."""
+    wl = I.WORKLOADS["tiny"]
+    ci = I.make_cache(wl)
+    qs, ks, vs = I.make_decode_inputs(wl, ci, wl.decode_steps)
+    cache = upload(ci)
+    K, V = f64(ci.k), f64(ci.v)
+    lens = ci.length.numpy().astype(np.int64).copy()
+    ws = torch.empty(B.decode_attn_workspace_size(cache, wl.n_q_heads), dtype=torch.uint8, device="cuda")
+    for s in range(wl.decode_steps):
+        out, lse = B.reco_decode_attn(cache, qs[s].cuda(), ks[s].cuda(), vs[s].cuda(), ws=ws)
+        ref, rl = oracle.decode_cache(K, V, lens, f64(qs[s]), 1 / np.sqrt(wl.head_dim), f64(ks[s]), f64(vs[s]))
+        assert_decode_close(out, ref, "f32", f"step {s}")
+        assert_lse_close(lse, rl, "f32", f"step {s}")
+    assert (cache.length.cpu().numpy() == lens).all()

@@ -1,0 +1,97 @@
+"""GPU parity of reco_logit_penalty (Eq. 3-4, bit-exact) and reco_answer_ppl (Eq. 5-6)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_04771_amd import binding as B
+from paper_2608_04771_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("rows,vocab,ld", [(1, 128256, 128256), (8, 152064, 152064), (5, 1000, 1037)])
+def test_penalty_bit_exact(rows, vocab, ld):
+    lo, hi = np.float32(0.4), np.float32(0.8)
+    edge = [np.float32(0.0), lo, np.nextafter(lo, np.float32(1)), np.float32(0.6),
+            np.nextafter(hi, np.float32(0)), hi, np.float32(1.0), np.float32(0.95)]
+    reward = np.array([edge[i % len(edge)] for i in range(rows)], dtype=np.float32)
+    ids = I.make_reflection_ids(64, vocab, seed=rows)
+    ids = np.concatenate([ids, ids[:5]])                          # duplicates must count once
+    full = I.make_logits(rows, ld, seed=vocab).numpy()
+    z = torch.from_numpy(full).cuda()
+    view = z[:, :vocab]
+    dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    B.reco_logit_penalty(view, torch.from_numpy(ids).cuda(), torch.from_numpy(reward).cuda(),
+                         float(lo), float(hi), 0.0, 1.0, 3.0, dev_err=dev_err)
+    torch.cuda.synchronize()
+    assert dev_err.item() == 0
+    ref = oracle.logit_penalty(full[:, :vocab], ids, reward, lo, hi, 0.0, 1.0, 3.0)
+    got = z.cpu().numpy()
+    assert got[:, :vocab].tobytes() == ref.tobytes()
+    assert got[:, vocab:].tobytes() == full[:, vocab:].tobytes()   # padding untouched
+
+
+def test_penalty_paper_form_and_bad_id():
+    vocab = 5000
+    beta = 3.0
+    z0 = I.make_logits(3, vocab, seed=1).numpy()
+    z = torch.from_numpy(z0.copy()).cuda()
+    ids = np.array([10, 20, 4999, -1, 5000, 30], dtype=np.int32)
+    reward = np.array([0.1, 0.5, 0.9], dtype=np.float32)
+    dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    B.reco_logit_penalty(z, torch.from_numpy(ids).cuda(), torch.from_numpy(reward).cuda(), 0.4, 0.8,
+                         0.0, beta / 2, beta, dev_err=dev_err)
+    torch.cuda.synchronize()
+    assert dev_err.item() == 4
+    good = [10, 20, 4999, 30]
+    ref = oracle.logit_penalty(z0, good, reward, 0.4, 0.8, 0.0, beta / 2, beta)
+    assert z.cpu().numpy().tobytes() == ref.tobytes()
+
+
+def _ppl_case(Bsz, n, vocab, seed, boost=None):
+    logits = I.make_logits(Bsz * n, vocab, seed=seed, shape=(Bsz, n, vocab))
+    tok = I.make_answer_tokens(Bsz, n, vocab, seed=seed + 1)
+    if boost is not None:
+        for b in boost:
+            logits[b, np.arange(n), tok[b]] += 25.0
+    return logits, tok
+
+
+@pytest.mark.parametrize("Bsz,n,vocab,boost", [(8, 32, 152064, (0, 3)), (2, 5, 1000, None), (1, 1, 17, (0,)),
+                                               (3, 7, 16385, (1,))])
+def test_answer_ppl_matches_oracle(Bsz, n, vocab, boost):
+    logits, tok = _ppl_case(Bsz, n, vocab, seed=vocab + n, boost=boost)
+    dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ppl, stop = B.reco_answer_ppl(logits.cuda(), torch.from_numpy(tok).cuda(), 1.1, dev_err=dev_err)
+    torch.cuda.synchronize()
+    assert dev_err.item() == 0
+    ref, rstop = oracle.answer_ppl(logits.numpy(), tok, 1.1)
+    g = ppl.cpu().numpy().astype(np.float64)
+    err = np.abs(np.log(g) - np.log(ref))
+    assert err.max() <= 1e-5, err.max()
+    for b in range(Bsz):
+        if abs(np.log(ref[b]) - np.log(np.float32(1.1))) > 1e-5:
+            assert bool(stop[b].item()) == bool(rstop[b])
+    if boost:
+        assert all(stop[b].item() == 1 for b in boost)
+
+
+def test_answer_ppl_uniform_logits_is_vocab():
+    vocab = 4096
+    logits = torch.zeros((2, 3, vocab), device="cuda")
+    tok = torch.zeros((2, 3), dtype=torch.int32, device="cuda")
+    ppl, stop = B.reco_answer_ppl(logits, tok, 1.1)
+    torch.cuda.synchronize()
+    assert np.allclose(ppl.cpu().numpy(), vocab, rtol=1e-6)
+    assert stop.cpu().tolist() == [0, 0]
+
+
+def test_answer_ppl_bad_token():
+    logits = torch.zeros((2, 3, 100), device="cuda")
+    tok = torch.tensor([[1, 2, 3], [4, 100, 5]], dtype=torch.int32, device="cuda")
+    dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ppl, _ = B.reco_answer_ppl(logits, tok, 1.1, dev_err=dev_err)
+    torch.cuda.synchronize()
+    assert dev_err.item() == 4
+    assert np.isnan(ppl[1].item()) and abs(ppl[0].item() - 100) < 1e-3

@@ -1,0 +1,106 @@
+"""End-to-end GPU parity of the hot path: score -> select/compact -> decode
+steps, on the tiny workload in full and on the 7B-shaped 16K workload at its
+full size in the launch configuration the bench times (all layers per call),
+checked on sampled units and steps."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import SCORE_RTOL, assert_decode_close, assert_lse_close, f64, kept_sets_match, upload
+from paper_2608_04771_amd import binding as B
+from paper_2608_04771_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def _compress_gpu(wl, ci, cache):
+    r = np.array([B.reco_retention_from_reward(float(v)) for v in ci.reward], dtype=np.float64)
+    scores = B.reco_score(cache, ci.q_win.cuda(), wl.window)
+    kept = torch.full(tuple(cache.shape[:4]), -1, dtype=torch.int32, device="cuda")
+    dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    B.reco_select_compact(cache, scores, torch.from_numpy(r).cuda(), wl.window, kept_idx=kept, dev_err=dev_err)
+    torch.cuda.synchronize()
+    assert dev_err.item() == 0
+    return r, scores.cpu().numpy(), kept.cpu().numpy()
+
+
+def test_tiny_workload_full_loop():
+    wl = I.WORKLOADS["tiny"]
+    ci = I.make_cache(wl)
+    cache = upload(ci)
+    K0, V0 = f64(ci.k), f64(ci.v)
+    r, s_gpu, kept = _compress_gpu(wl, ci, cache)
+    s_or = oracle.score_cache(K0, ci.length.numpy(), f64(ci.q_win), 1 / np.sqrt(wl.head_dim))
+    # the oracle's own compression
+    _, idx_or, K, V, lens = oracle.compress_cache(K0, V0, ci.length.numpy().astype(np.int64), f64(ci.q_win), r,
+                                                  wl.window, 1 / np.sqrt(wl.head_dim))
+    exact = True
+    for h in range(wl.n_kv_heads):
+        L = int(ci.seq_len[0])
+        ok, msg = kept_sets_match(kept[0, 0, h], s_or[0, 0, h], L, wl.window, r[0])
+        assert ok, msg
+        exact = exact and msg == "exact"
+        m = len(idx_or[(0, 0, h)])
+        if msg != "exact":
+            # continue from the GPU's (equally valid) selection
+            K[0, 0, h, :m] = K0[0, 0, h][kept[0, 0, h, :m]]
+            V[0, 0, h, :m] = V0[0, 0, h][kept[0, 0, h, :m]]
+    assert (cache.length.cpu().numpy() == lens).all()
+    assert np.array_equal(f64(cache.k)[..., :int(lens.max()), :], K[..., :int(lens.max()), :])
+    qs, ks, vs = I.make_decode_inputs(wl, ci, wl.decode_steps)
+    for s in range(wl.decode_steps):
+        out, lse = B.reco_decode_attn(cache, qs[s].cuda(), ks[s].cuda(), vs[s].cuda())
+        ref, rl = oracle.decode_cache(K, V, lens, f64(qs[s]), 1 / np.sqrt(wl.head_dim), f64(ks[s]), f64(vs[s]))
+        assert_decode_close(out, ref, "f32", f"step {s}")
+        assert_lse_close(lse, rl, "f32", f"step {s}")
+    print("tiny loop: selection", "exact" if exact else "with excused ties")
+
+
+def test_7b16k_full_size_sampled():
+    """28 layers x 4 KV heads, 16,384 cached tokens, bf16: every call covers all
+    layers (the bench's launch configuration).  Sampled units are checked
+    against the oracle for scores, kept sets, gathered rows and decode steps;
+    all units are checked for lengths and finiteness."""
+    wl = I.WORKLOADS["7b16k"]
+    ci = I.make_cache(wl)
+    cache = upload(ci)
+    k_before = cache.k.clone()
+    r, s_gpu, kept = _compress_gpu(wl, ci, cache)
+    L = int(ci.seq_len[0])
+    m = oracle.kept_count(L, wl.window, float(r[0]))
+    assert (cache.length.cpu().numpy() == m).all()
+    G = wl.group
+    scale = 1 / np.sqrt(wl.head_dim)
+    units = [(0, 0, 0), (5, 0, 3), (13, 0, 1), (27, 0, 2)]
+    for (l, b, h) in units:
+        Kf = f64(ci.k[l, b, h, :L])
+        s_or = oracle.score_unit(Kf, f64(ci.q_win[l, b, h * G:(h + 1) * G]), scale)
+        rel = np.abs(s_gpu[l, b, h, :L] - s_or) / s_or
+        assert rel.max() <= SCORE_RTOL, rel.max()
+        ok, msg = kept_sets_match(kept[l, b, h], s_or, L, wl.window, float(r[0]))
+        assert ok, msg
+        idx = torch.from_numpy(kept[l, b, h, :m].astype(np.int64)).cuda()
+        assert torch.equal(cache.k[l, b, h, :m], k_before[l, b, h][idx])
+    # gathered rows of every unit are bit-exact copies
+    kk = torch.from_numpy(kept[..., :m].astype(np.int64)).cuda()
+    gathered = torch.gather(k_before, 3, kk[..., None].expand(-1, -1, -1, -1, wl.head_dim))
+    assert torch.equal(cache.k[:, :, :, :m], gathered)
+    del gathered, k_before
+    steps = wl.decode_steps
+    qs, ks, vs = I.make_decode_inputs(wl, ci, steps)
+    check_steps = {0, steps // 2, steps - 1}
+    ws = torch.empty(B.decode_attn_workspace_size(cache, wl.n_q_heads), dtype=torch.uint8, device="cuda")
+    for s in range(steps):
+        out, lse = B.reco_decode_attn(cache, qs[s].cuda(), ks[s].cuda(), vs[s].cuda(), ws=ws)
+        if s in check_steps:
+            torch.cuda.synchronize()
+            assert torch.isfinite(out.float()).all()
+            for (l, b, h) in units:
+                n = m + s + 1                       # the call appended row m + s
+                Kc = f64(cache.k[l, b, h, :n])
+                Vc = f64(cache.v[l, b, h, :n])
+                ref, rl = oracle.decode_unit(Kc, Vc, n, f64(qs[s][l, b, h * G:(h + 1) * G]), scale)
+                assert_decode_close(out[l, b, h * G:(h + 1) * G], ref, "bf16", f"step {s} unit {(l, b, h)}")
+                assert_lse_close(lse[l, b, h * G:(h + 1) * G], rl, "bf16", f"step {s} unit {(l, b, h)}")
+    assert (cache.length.cpu().numpy() == m + steps).all()

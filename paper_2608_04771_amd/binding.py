@@ -151,10 +151,17 @@ def answer_ppl_workspace_size(batch: int, n: int, vocab: int) -> int:
     return int(load_library().reco_answer_ppl_workspace_size(batch, n, vocab))
 
 
-def _ws(nbytes: int, device, ws: Optional[torch.Tensor]) -> torch.Tensor:
+def _ws(nbytes: int, device, ws: Optional[torch.Tensor], zero: bool = False) -> torch.Tensor:
     if ws is not None:
         return ws
-    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+    alloc = torch.zeros if zero else torch.empty
+    return alloc(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def decode_workspace(cache: "KVCache", n_q_heads: int, n_layers: Optional[int] = None) -> torch.Tensor:
+    """A zero-filled decode workspace (its completion counters must start at 0;
+    every call leaves them at 0 again).  Do not share one between overlapping calls."""
+    return _ws(decode_attn_workspace_size(cache, n_q_heads, n_layers), cache.k.device, None, zero=True)
 
 
 def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[float] = None, causal: bool = True,
@@ -216,7 +223,7 @@ def reco_decode_attn(cache: KVCache, q: torch.Tensor, k_new: Optional[torch.Tens
     if lse is None and want_lse:
         lse = torch.empty((nl, B, hq), dtype=torch.float32, device=q.device)
     _need_cuda(q, k_new, v_new, out, lse, ws, dev_err)
-    ws = _ws(decode_attn_workspace_size(cache, hq, nl), q.device, ws)
+    ws = _ws(decode_attn_workspace_size(cache, hq, nl), q.device, ws, zero=True)
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     st = load_library().reco_decode_attn(cache.ref(), layer0, nl, _ptr(q), hq, scale, _ptr(k_new), _ptr(v_new),
                                          _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _ptr(dev_err),

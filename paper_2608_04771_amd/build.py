@@ -52,7 +52,7 @@ def build_library(verbose: bool = False) -> str:
                            "-c", os.path.join(CSRC, src), "-o", obj]))
     for src in HOST_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
-        jobs.append((obj, [hipcc, *common, "-c", os.path.join(CSRC, src), "-o", obj]))
+        jobs.append((obj, [hipcc, f"--offload-arch={ARCH}", *common, "-c", os.path.join(CSRC, src), "-o", obj]))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
         outs = list(ex.map(lambda j: _run(j[1]), jobs))
     if verbose:

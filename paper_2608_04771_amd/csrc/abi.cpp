@@ -1,7 +1,7 @@
 // C ABI of the library: host-side argument validation, workspace sizing and
 // launches.  Every entry point validates everything it can see on the host
 // before launching anything, so a non-OK status means no side effects.
-#include "../../include/reco.h"
+#include "reco.h"
 
 #include <hip/hip_runtime.h>
 #include <math.h>

@@ -12,8 +12,12 @@
 // operand needs (same lane, same element slot), so P never leaves registers;
 // V is staged through LDS to read it column-wise.  Softmax is online in the
 // log2 domain with fp32 statistics.  The four waves' (max, sum, O) states are
-// merged through LDS and written as one split partial; a second kernel merges
-// the splits, writes out / lse and commits the optional append.
+// merged through LDS and written as one split partial.  A second kernel
+// merges the splits of each unit, writes out / lse and commits the optional
+// append (so no workgroup of the attention kernel races on len).  Merging in
+// the last-finishing workgroup instead would need device-scope fences, which
+// on this chip write back and invalidate the L2 that the streaming
+// workgroups depend on.
 #include "reco_device.hpp"
 #include "reco_kernels.hpp"
 
@@ -26,6 +30,7 @@ namespace {
 constexpr int kTile = 32;        // keys per wave iteration
 constexpr int kWavesPerWG = 4;
 constexpr int kThreads = kWavesPerWG * kWave;
+constexpr int kMaxSplits = 128;
 
 template <typename T, int D>
 struct DecodeCfg {
@@ -40,8 +45,53 @@ struct DecodeCfg {
   static constexpr int stage_bytes = kWavesPerWG * kTile * lds_stride;
   static constexpr int merge_bytes = kWavesPerWG * (32 + 16 * D) * 4;
   static constexpr int smem_bytes = stage_bytes > merge_bytes ? stage_bytes : merge_bytes;
-  static constexpr int vload_u4 = row_bytes / 2 / 16;  // uint4 per lane for half a V row
+  // Coalesced tile loads: per instruction the wave reads 1 KB of consecutive
+  // rows (lane l takes 16 bytes at l * 16), so every 128-byte line is read whole.
+  static constexpr int lanes_per_row = row_bytes / 16;
+  static constexpr int rows_per_inst = kWave / lanes_per_row;
+  static constexpr int v_insts = kTile / rows_per_inst;
+  // Two workgroups per CU (two waves per SIMD) where the double-buffered
+  // tile fits in 256 registers; the fp32 head_dim-128 variant needs more.
+  static constexpr int min_wgs = (sizeof(T) == 4 && D == 128) ? 1 : 2;
 };
+
+// Registers of one 32-key tile: K already in MFMA operand layout, V as
+// coalesced 16-byte pieces bound for the LDS stage.
+template <typename T, int D>
+struct TileRegs {
+  typename Mfma<T>::frag kf[2][DecodeCfg<T, D>::qk_steps];
+  uint4 vreg[DecodeCfg<T, D>::v_insts];
+};
+
+// Issue the loads of the tile starting at key kb.  Keys >= n_cache come from
+// the appended row (key == n_cache) or are zero; every address stays inside
+// the unit (rows past the end read row 0 and are masked or zeroed).
+template <typename T, int D>
+__device__ __forceinline__ void load_tile(TileRegs<T, D> &tr, int kb, int n_cache, bool append, const T *kbase,
+                                          const T *vbase, const T *knew, const T *vnew, int lane) {
+  using Cfg = DecodeCfg<T, D>;
+  const int col = lane & 15, grp = lane >> 4;
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf) {
+    const int key = kb + hf * 16 + col;
+    const T *row = key < n_cache ? kbase + static_cast<size_t>(key) * D
+                                 : ((key == n_cache && append) ? knew : kbase);
+    row += grp * Cfg::dq;
+#pragma unroll
+    for (int c = 0; c < Cfg::qk_steps; ++c) tr.kf[hf][c] = load_frag(row + c * Cfg::kpl);
+  }
+#pragma unroll
+  for (int i = 0; i < Cfg::v_insts; ++i) {
+    const int r = i * Cfg::rows_per_inst + lane / Cfg::lanes_per_row;
+    const int key = kb + r;
+    const bool in_cache = key < n_cache;
+    const bool is_new = key == n_cache && append;
+    const T *row = in_cache ? vbase + static_cast<size_t>(key) * D : (is_new ? vnew : vbase);
+    const uint4 x = *reinterpret_cast<const uint4 *>(reinterpret_cast<const unsigned char *>(row) +
+                                                    (lane % Cfg::lanes_per_row) * 16);
+    tr.vreg[i] = (in_cache || is_new) ? x : make_uint4(0, 0, 0, 0);
+  }
+}
 
 template <typename T>
 __device__ __forceinline__ T lds_elem(const unsigned char *p) {
@@ -82,7 +132,7 @@ __device__ __forceinline__ typename Mfma<T>::frag pt_frag(const float (&pv)[8], 
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) {
+__global__ __launch_bounds__(kThreads, (DecodeCfg<T, D>::min_wgs)) void decode_split_kernel(DecodeParams p) {
   using Cfg = DecodeCfg<T, D>;
   using MF = Mfma<T>;
   using frag = typename MF::frag;
@@ -133,36 +183,16 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) 
 
   unsigned char *stage = smem + wave * kTile * Cfg::lds_stride;
 
+  TileRegs<T, D> cur;
+  if (t0 + wave < t1) load_tile<T, D>(cur, (t0 + wave) * kTile, n_cache, append, kbase, vbase, knew, vnew, lane);
   for (int t = t0 + wave; t < t1; t += kWavesPerWG) {
     const int kb = t * kTile;
-    // K operand: lane holds key kb + hf*16 + col, head-dim slice of its group.
-    frag kf[2][Cfg::qk_steps];
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      const int key = kb + hf * 16 + col;
-      const T *row = key < n_cache ? kbase + static_cast<size_t>(key) * D
-                                   : ((key == n_cache && append) ? knew : kbase);
-      row += grp * Cfg::dq;
-#pragma unroll
-      for (int c = 0; c < Cfg::qk_steps; ++c) kf[hf][c] = load_frag(row + c * Cfg::kpl);
-    }
-    // V rows for the stage: lane -> row lane/2, half lane%2 (rows past the end are zero).
-    uint4 vreg[Cfg::vload_u4];
-    {
-      const int r = lane >> 1;
-      const int key = kb + r;
-      const T *row = key < n_cache ? vbase + static_cast<size_t>(key) * D
-                                   : ((key == n_cache && append) ? vnew : nullptr);
-      if (row) {
-        const uint4 *src = reinterpret_cast<const uint4 *>(reinterpret_cast<const unsigned char *>(row) +
-                                                           (lane & 1) * (Cfg::row_bytes / 2));
-#pragma unroll
-        for (int i = 0; i < Cfg::vload_u4; ++i) vreg[i] = src[i];
-      } else {
-#pragma unroll
-        for (int i = 0; i < Cfg::vload_u4; ++i) vreg[i] = make_uint4(0, 0, 0, 0);
-      }
-    }
+    // Prefetch this wave's next tile (the last iteration re-reads its own
+    // tile, which stays cached) so loads are in flight during the compute.
+    TileRegs<T, D> nxt;
+    const int tn = min(t + kWavesPerWG, t1 - 1);
+    load_tile<T, D>(nxt, tn * kTile, n_cache, append, kbase, vbase, knew, vnew, lane);
+    const auto &kf = cur.kf;
 
     // S^T = K . Q^T for the two 16-key halves.
     f32x4_t s[2];
@@ -204,13 +234,12 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) 
     }
 
     // Stage V (row-major, padded pitch) and read it back column-wise.
-    {
-      uint2 *dst = reinterpret_cast<uint2 *>(stage + (lane >> 1) * Cfg::lds_stride + (lane & 1) * (Cfg::row_bytes / 2));
 #pragma unroll
-      for (int i = 0; i < Cfg::vload_u4; ++i) {
-        dst[2 * i] = make_uint2(vreg[i].x, vreg[i].y);
-        dst[2 * i + 1] = make_uint2(vreg[i].z, vreg[i].w);
-      }
+    for (int i = 0; i < Cfg::v_insts; ++i) {
+      const int r = i * Cfg::rows_per_inst + lane / Cfg::lanes_per_row;
+      uint2 *dst = reinterpret_cast<uint2 *>(stage + r * Cfg::lds_stride + (lane % Cfg::lanes_per_row) * 16);
+      dst[0] = make_uint2(cur.vreg[i].x, cur.vreg[i].y);
+      dst[1] = make_uint2(cur.vreg[i].z, cur.vreg[i].w);
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
@@ -222,6 +251,7 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) 
       }
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    cur = nxt;
   }
 
   // Total of the per-lane partial sums of query col.
@@ -268,60 +298,85 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(DecodeParams p) 
       pml[16 + qi] = L;
     }
   }
+
 }
 
-// Merge the split partials of one unit, write out / lse and commit the append.
+// Merge the split partials of every (unit, query head), write out / lse and
+// commit the append.  One 64-lane wave per (unit, query head): every lane
+// fetches all split statistics at once (one memory round trip), derives the
+// merge weights itself, then loads its head-dim slice of every split partial
+// (a second round trip).  The appended row is fetched up front.
 template <typename T, int D>
-__global__ __launch_bounds__(256) void decode_merge_kernel(DecodeParams p) {
+__global__ __launch_bounds__(kWave) void decode_merge_kernel(DecodeParams p) {
+  constexpr int kPer = D / kWave;                  // head-dim elements per lane
   const int unit = blockIdx.x;
+  const int qi = blockIdx.y;
+  const int lane = threadIdx.x;
   const int per_layer = p.batch * p.hkv;
   const int lc = unit / per_layer;
   const int b = (unit % per_layer) / p.hkv;
   const int h = unit % p.hkv;
   const size_t cunit = (static_cast<size_t>(p.layer0 + lc) * p.batch + b) * p.hkv + h;
   const size_t qunit = static_cast<size_t>(lc) * per_layer + static_cast<size_t>(b) * p.hkv + h;
-  const int len_in = p.len[cunit];
-  const bool append = p.k_new != nullptr;
+  const int S = p.splits;
+  const bool append = p.k_new != nullptr && qi == 0;
 
-  const float *pml = p.part_ml + static_cast<size_t>(unit) * p.splits * 32;
-  const float *po = p.part_o + static_cast<size_t>(unit) * p.splits * 16 * D;
-  T *out = reinterpret_cast<T *>(p.out) + ((static_cast<size_t>(lc) * p.batch + b) * p.hq + h * p.group) * D;
-  for (int idx = threadIdx.x; idx < p.group * D; idx += blockDim.x) {
-    const int qi = idx / D;
-    const int d = idx - qi * D;
-    float M = -INFINITY;
-    for (int s = 0; s < p.splits; ++s) M = fmaxf(M, pml[s * 32 + qi]);
-    float L = 0.f, acc = 0.f;
-    if (M != -INFINITY) {
-      for (int s = 0; s < p.splits; ++s) {
-        const float wgt = fast_exp2(pml[s * 32 + qi] - M);
-        L += pml[s * 32 + 16 + qi] * wgt;
-        acc += po[(static_cast<size_t>(s) * 16 + qi) * D + d] * wgt;
-      }
-    }
-    out[static_cast<size_t>(qi) * D + d] = from_f32<T>(L > 0.f ? acc / L : 0.f);
-    if (d == 0 && p.lse) {
-      p.lse[(static_cast<size_t>(lc) * p.batch + b) * p.hq + h * p.group + qi] =
-          L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+  // Query head 0 of the unit also commits the append: fetch the row now.
+  T krow[kPer], vrow[kPer];
+  if (append) {
+    const T *ksrc = reinterpret_cast<const T *>(p.k_new) + qunit * D;
+    const T *vsrc = reinterpret_cast<const T *>(p.v_new) + qunit * D;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      krow[i] = ksrc[lane + i * kWave];
+      vrow[i] = vsrc[lane + i * kWave];
     }
   }
+  const float *pml = p.part_ml + static_cast<size_t>(unit) * S * 32;
+  // Lane s holds split s's statistics, lane s - 64 the rest (S <= kMaxSplits = 128).
+  const float m0 = lane < S ? pml[lane * 32 + qi] : -INFINITY;
+  const float l0 = lane < S ? pml[lane * 32 + 16 + qi] : 0.f;
+  const float m1 = lane + kWave < S ? pml[(lane + kWave) * 32 + qi] : -INFINITY;
+  const float l1 = lane + kWave < S ? pml[(lane + kWave) * 32 + 16 + qi] : 0.f;
+  const float M = wave_max(fmaxf(m0, m1));
+  float L = 0.f;
+  if (M != -INFINITY) L = wave_sum(l0 * fast_exp2(m0 - M) + l1 * fast_exp2(m1 - M));
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  const float w0 = (M != -INFINITY) ? fast_exp2(m0 - M) * inv : 0.f;
+  const float w1 = (M != -INFINITY) ? fast_exp2(m1 - M) * inv : 0.f;
 
-  if (threadIdx.x == 0 && (len_in < 0 || len_in > p.cap)) report(p.dev_err, 5 /*RECO_DEV_BAD_LENGTH*/);
+  const float *po = p.part_o + (static_cast<size_t>(unit) * S * 16 + qi) * D;
+  float acc[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) acc[i] = 0.f;
+  for (int s = 0; s < S; ++s) {
+    const float wgt = __shfl(s < kWave ? w0 : w1, s & (kWave - 1), kWave);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) acc[i] += wgt * po[static_cast<size_t>(s) * 16 * D + lane + i * kWave];
+  }
+  T *out = reinterpret_cast<T *>(p.out) + ((static_cast<size_t>(lc) * p.batch + b) * p.hq + h * p.group + qi) * D;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) out[lane + i * kWave] = from_f32<T>(acc[i]);
+  if (p.lse && lane == 0)
+    p.lse[(static_cast<size_t>(lc) * p.batch + b) * p.hq + h * p.group + qi] =
+        L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+
+  if (qi != 0) return;
+  const int len_in = p.len[cunit];
+  if (lane == 0 && (len_in < 0 || len_in > p.cap)) report(p.dev_err, 5 /*RECO_DEV_BAD_LENGTH*/);
   if (!append || len_in < 0 || len_in > p.cap) return;
   if (len_in == p.cap) {
-    if (threadIdx.x == 0) report(p.dev_err, 1 /*RECO_DEV_APPEND_OVERFLOW*/);
+    if (lane == 0) report(p.dev_err, 1 /*RECO_DEV_APPEND_OVERFLOW*/);
     return;
   }
   T *kdst = reinterpret_cast<T *>(p.k) + (cunit * p.cap + len_in) * D;
   T *vdst = reinterpret_cast<T *>(p.v) + (cunit * p.cap + len_in) * D;
-  const T *ksrc = reinterpret_cast<const T *>(p.k_new) + qunit * D;
-  const T *vsrc = reinterpret_cast<const T *>(p.v_new) + qunit * D;
-  for (int d = threadIdx.x; d < D; d += blockDim.x) {
-    kdst[d] = ksrc[d];
-    vdst[d] = vsrc[d];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    kdst[lane + i * kWave] = krow[i];
+    vdst[lane + i * kWave] = vrow[i];
   }
-  __syncthreads();
-  if (threadIdx.x == 0) p.len[cunit] = len_in + 1;
+  if (lane == 0) p.len[cunit] = len_in + 1;
 }
 
 template <typename T, int D>
@@ -330,19 +385,23 @@ hipError_t launch_typed(const DecodeParams &p, hipStream_t s) {
   hipLaunchKernelGGL((decode_split_kernel<T, D>), dim3(p.splits, units), dim3(kThreads), 0, s, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((decode_merge_kernel<T, D>), dim3(units), dim3(256), 0, s, p);
+  hipLaunchKernelGGL((decode_merge_kernel<T, D>), dim3(units, p.group), dim3(kWave), 0, s, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
-// Splits per unit: aim for a few thousand workgroups over the chip while
-// keeping at least four 32-key tiles per workgroup at full capacity.
+// Splits per unit: fill the chip with one round of workgroups.  MI355X has
+// 256 CUs and the bf16 kernel runs two workgroups per CU, so up to 512
+// workgroups are resident at once; with U units, floor(512 / U) splits keep
+// every workgroup resident (no tail round) while each one streams a long
+// contiguous run of keys.  At least four 32-key tiles per split at capacity.
 int decode_splits(int units, int capacity) {
-  const int target_wgs = 2048;
+  const int resident_wgs = 2 * 256;
   const int tiles_cap = (capacity + 1 + kTile - 1) / kTile;
-  int splits = (target_wgs + units - 1) / units;
+  int splits = resident_wgs / units;
   int max_splits = tiles_cap / 4;
+  if (max_splits > kMaxSplits) max_splits = kMaxSplits;
   if (max_splits < 1) max_splits = 1;
   if (splits > max_splits) splits = max_splits;
   if (splits < 1) splits = 1;

@@ -10,26 +10,30 @@ namespace reco {
 
 namespace {
 
-constexpr int kPenThreads = 64;
+constexpr int kPenThreads = 256;
+constexpr int kMaxIds = 4096;
 
 __global__ __launch_bounds__(kPenThreads) void logit_penalty_kernel(float *logits, int vocab, int64_t ld,
                                                                     const int32_t *ids, int n_ids,
                                                                     const float *reward, float tau_lo,
                                                                     float tau_hi, float b_lo, float b_mid,
                                                                     float b_hi, int32_t *dev_err) {
+  __shared__ int32_t s_ids[kMaxIds];
   const int row = blockIdx.x;
+  for (int i = threadIdx.x; i < n_ids; i += kPenThreads) s_ids[i] = ids[i];
+  __syncthreads();
   const float v = reward[row];
   // Eq. 3 exactly as written: v <= tau_lo, tau_lo < v < tau_hi, v >= tau_hi.
   const float beta = (v <= tau_lo) ? b_lo : ((v >= tau_hi) ? b_hi : b_mid);
   float *z = logits + static_cast<int64_t>(row) * ld;
   for (int i = threadIdx.x; i < n_ids; i += kPenThreads) {
-    const int u = ids[i];
+    const int u = s_ids[i];
     if (u < 0 || u >= vocab) {
       report(dev_err, 4 /*RECO_DEV_BAD_TOKEN_ID*/);
       continue;
     }
     bool first = true;  // R is a set: only the first occurrence of an id subtracts
-    for (int j = 0; j < i; ++j) first = first && (ids[j] != u);
+    for (int j = 0; j < i; ++j) first = first && (s_ids[j] != u);
     if (first) z[u] = z[u] - beta;
   }
 }

@@ -99,7 +99,7 @@ def test_decode_tiny_workload_64_steps():
     cache = upload(ci)
     K, V = f64(ci.k), f64(ci.v)
     lens = ci.length.numpy().astype(np.int64).copy()
-    ws = torch.empty(B.decode_attn_workspace_size(cache, wl.n_q_heads), dtype=torch.uint8, device="cuda")
+    ws = B.decode_workspace(cache, wl.n_q_heads)
     for s in range(wl.decode_steps):
         out, lse = B.reco_decode_attn(cache, qs[s].cuda(), ks[s].cuda(), vs[s].cuda(), ws=ws)
         ref, rl = oracle.decode_cache(K, V, lens, f64(qs[s]), 1 / np.sqrt(wl.head_dim), f64(ks[s]), f64(vs[s]))

@@ -90,7 +90,7 @@ def test_7b16k_full_size_sampled():
     steps = wl.decode_steps
     qs, ks, vs = I.make_decode_inputs(wl, ci, steps)
     check_steps = {0, steps // 2, steps - 1}
-    ws = torch.empty(B.decode_attn_workspace_size(cache, wl.n_q_heads), dtype=torch.uint8, device="cuda")
+    ws = B.decode_workspace(cache, wl.n_q_heads)
     for s in range(steps):
         out, lse = B.reco_decode_attn(cache, qs[s].cuda(), ks[s].cuda(), vs[s].cuda(), ws=ws)
         if s in check_steps:

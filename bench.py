@@ -295,7 +295,7 @@ def main():
         "phase_ms": {"score": float(score_ms.mean()), "select_compact": float(sel_ms.mean()),
                      "compress": float(comp_ms.mean()), "decode_call": dec_avg_ms,
                      "decode_calls_total": float(dec_loop_ms.mean()), "answer_ppl": float(ppl_ms.mean())},
-        "roofline": {"kernel": "reco_decode_attn (decode_split_kernel, merge fused)", "bound": "hbm",
+        "roofline": {"kernel": "reco_decode_attn (decode_split_kernel + decode_merge_kernel)", "bound": "hbm",
                      "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
                      "traffic": None, "algorithmic_bytes_per_launch": dec_bytes_mean},
     }

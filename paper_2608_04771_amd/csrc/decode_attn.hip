@@ -9,8 +9,10 @@
 //   S^T = K_tile . Q^T            (M = 16 keys per half, N = 16 padded queries)
 //   O^T += V_tile^T . P^T         (M = 16 head-dim rows per d-tile, N = 16 queries)
 // The S^T accumulator already holds, per lane, the probabilities the P^T
-// operand needs (same lane, same element slot), so P never leaves registers;
-// V is staged through LDS to read it column-wise.  Softmax is online in the
+// operand needs (same lane, same element slot), so P never leaves registers.
+// K and V are streamed with coalesced non-temporal 16-byte loads (each 128-byte
+// line read whole, nothing allocated in L2) and staged through LDS: K is
+// re-read in the MFMA operand layout, V column-wise.  Softmax is online in the
 // log2 domain with fp32 statistics.  The four waves' (max, sum, O) states are
 // merged through LDS and written as one split partial.  A second kernel
 // merges the splits of each unit, writes out / lse and commits the optional
@@ -42,7 +44,9 @@ struct DecodeCfg {
   static constexpr int pv_ops = kTile / MF::kPerOp;  // MFMAs per d-tile per 32-key tile
   static constexpr int row_bytes = D * (int)sizeof(T);
   static constexpr int lds_stride = row_bytes + 8;  // padded row pitch of the V stage
-  static constexpr int stage_bytes = kWavesPerWG * kTile * lds_stride;
+  static constexpr int k_stride = row_bytes + 16;   // padded, 16-byte aligned pitch of the K stage
+  static constexpr int wave_stage = kTile * (lds_stride + k_stride);
+  static constexpr int stage_bytes = kWavesPerWG * wave_stage;
   static constexpr int merge_bytes = kWavesPerWG * (32 + 16 * D) * 4;
   static constexpr int smem_bytes = stage_bytes > merge_bytes ? stage_bytes : merge_bytes;
   // Coalesced tile loads: per instruction the wave reads 1 KB of consecutive
@@ -55,11 +59,11 @@ struct DecodeCfg {
   static constexpr int min_wgs = (sizeof(T) == 4 && D == 128) ? 1 : 2;
 };
 
-// Registers of one 32-key tile: K already in MFMA operand layout, V as
-// coalesced 16-byte pieces bound for the LDS stage.
+// Registers of one 32-key tile: K and V as coalesced 16-byte pieces bound
+// for the LDS stages (K is re-read from LDS in the MFMA operand layout).
 template <typename T, int D>
 struct TileRegs {
-  typename Mfma<T>::frag kf[2][DecodeCfg<T, D>::qk_steps];
+  uint4 kreg[DecodeCfg<T, D>::v_insts];
   uint4 vreg[DecodeCfg<T, D>::v_insts];
 };
 
@@ -70,26 +74,20 @@ template <typename T, int D>
 __device__ __forceinline__ void load_tile(TileRegs<T, D> &tr, int kb, int n_cache, bool append, const T *kbase,
                                           const T *vbase, const T *knew, const T *vnew, int lane) {
   using Cfg = DecodeCfg<T, D>;
-  const int col = lane & 15, grp = lane >> 4;
-#pragma unroll
-  for (int hf = 0; hf < 2; ++hf) {
-    const int key = kb + hf * 16 + col;
-    const T *row = key < n_cache ? kbase + static_cast<size_t>(key) * D
-                                 : ((key == n_cache && append) ? knew : kbase);
-    row += grp * Cfg::dq;
-#pragma unroll
-    for (int c = 0; c < Cfg::qk_steps; ++c) tr.kf[hf][c] = load_frag(row + c * Cfg::kpl);
-  }
+  const int sub = (lane % Cfg::lanes_per_row) * 16;
 #pragma unroll
   for (int i = 0; i < Cfg::v_insts; ++i) {
     const int r = i * Cfg::rows_per_inst + lane / Cfg::lanes_per_row;
     const int key = kb + r;
     const bool in_cache = key < n_cache;
     const bool is_new = key == n_cache && append;
-    const T *row = in_cache ? vbase + static_cast<size_t>(key) * D : (is_new ? vnew : vbase);
-    const uint4 x = *reinterpret_cast<const uint4 *>(reinterpret_cast<const unsigned char *>(row) +
-                                                    (lane % Cfg::lanes_per_row) * 16);
-    tr.vreg[i] = (in_cache || is_new) ? x : make_uint4(0, 0, 0, 0);
+    const size_t off = in_cache ? static_cast<size_t>(key) * D : 0;
+    const T *krow = is_new ? knew : kbase + off;
+    const T *vrow = is_new ? vnew : vbase + off;
+    const uint4 kx = nt_load_u4(reinterpret_cast<const unsigned char *>(krow) + sub);
+    const uint4 vx = nt_load_u4(reinterpret_cast<const unsigned char *>(vrow) + sub);
+    tr.kreg[i] = kx;                                       // rows past the end are masked
+    tr.vreg[i] = (in_cache || is_new) ? vx : make_uint4(0, 0, 0, 0);
   }
 }
 
@@ -181,7 +179,8 @@ __global__ __launch_bounds__(kThreads, (DecodeCfg<T, D>::min_wgs)) void decode_s
 #pragma unroll
   for (int dt = 0; dt < Cfg::dtiles; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  unsigned char *stage = smem + wave * kTile * Cfg::lds_stride;
+  unsigned char *stage = smem + wave * Cfg::wave_stage;           // V, row pitch lds_stride
+  unsigned char *kstage = stage + kTile * Cfg::lds_stride;          // K, row pitch k_stride
 
   TileRegs<T, D> cur;
   if (t0 + wave < t1) load_tile<T, D>(cur, (t0 + wave) * kTile, n_cache, append, kbase, vbase, knew, vnew, lane);
@@ -192,7 +191,21 @@ __global__ __launch_bounds__(kThreads, (DecodeCfg<T, D>::min_wgs)) void decode_s
     TileRegs<T, D> nxt;
     const int tn = min(t + kWavesPerWG, t1 - 1);
     load_tile<T, D>(nxt, tn * kTile, n_cache, append, kbase, vbase, knew, vnew, lane);
-    const auto &kf = cur.kf;
+    // K tile -> LDS -> MFMA operand layout (lane holds key hf*16 + col,
+    // head-dim slice grp*dq + c*kpl of it).
+#pragma unroll
+    for (int i = 0; i < Cfg::v_insts; ++i) {
+      const int r = i * Cfg::rows_per_inst + lane / Cfg::lanes_per_row;
+      *reinterpret_cast<uint4 *>(kstage + r * Cfg::k_stride + (lane % Cfg::lanes_per_row) * 16) = cur.kreg[i];
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    frag kf[2][Cfg::qk_steps];
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const T *krow = reinterpret_cast<const T *>(kstage + (hf * 16 + col) * Cfg::k_stride) + grp * Cfg::dq;
+#pragma unroll
+      for (int c = 0; c < Cfg::qk_steps; ++c) kf[hf][c] = load_frag(krow + c * Cfg::kpl);
+    }
 
     // S^T = K . Q^T for the two 16-key halves.
     f32x4_t s[2];
@@ -391,15 +404,15 @@ hipError_t launch_typed(const DecodeParams &p, hipStream_t s) {
 
 }  // namespace
 
-// Splits per unit: fill the chip with one round of workgroups.  MI355X has
-// 256 CUs and the bf16 kernel runs two workgroups per CU, so up to 512
-// workgroups are resident at once; with U units, floor(512 / U) splits keep
-// every workgroup resident (no tail round) while each one streams a long
-// contiguous run of keys.  At least four 32-key tiles per split at capacity.
+// Splits per unit: at most one workgroup per compute unit (MI355X has 256).
+// Measured on the 7B-shaped cache, a single resident round with one
+// workgroup per CU streams fastest: two workgroups sharing a CU finish later
+// than the rest, and a second round adds its ramp to the tail.  At least
+// four 32-key tiles per split at capacity.
 int decode_splits(int units, int capacity) {
-  const int resident_wgs = 2 * 256;
+  const int compute_units = 256;
   const int tiles_cap = (capacity + 1 + kTile - 1) / kTile;
-  int splits = resident_wgs / units;
+  int splits = compute_units / units;
   int max_splits = tiles_cap / 4;
   if (max_splits > kMaxSplits) max_splits = kMaxSplits;
   if (max_splits < 1) max_splits = 1;

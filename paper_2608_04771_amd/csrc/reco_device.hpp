@@ -64,6 +64,13 @@ struct Mfma<float> {
   }
 };
 
+// 16-byte load that does not allocate in the caches (streamed data read once).
+typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 nt_load_u4(const void *p) {
+  const u32x4v w = __builtin_nontemporal_load(reinterpret_cast<const u32x4v *>(p));
+  return make_uint4(w.x, w.y, w.z, w.w);
+}
+
 // Load kPerLane consecutive elements starting at p as one MFMA fragment.
 __device__ __forceinline__ bf16x8_t load_frag(const bf16_t *p) {
   uint4 u = *reinterpret_cast<const uint4 *>(p);

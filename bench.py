@@ -37,6 +37,31 @@ BETAS = (0.0, 1.0, 3.0)                        # penalty per reward band
 N_REFL = 64
 ANSWER_LEN = 32
 
+# HBM traffic of one decode_split_kernel launch on this workload, from two
+# rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE), each scaled by what the
+# counter reads for a plain device copy of known size (factors 0.5001 and
+# 1.0000).  Valid only for the kernel sources it was taken with: if those
+# files change, the figure is reported as null until it is measured again.
+DECODE_TRAFFIC = {
+    "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
+                "paper_2608_04771_amd/csrc/reco_kernels.hpp"),
+    "sha256": "52af6de82fb9a3abb109ebb45eb7b605b98a1f001936a12147e55d3b24044f39",
+    "workload": "7b-28L-28q4kv-d128-bf16-L16384",
+    "fetch_bytes": 555355048,
+    "write_bytes": 817152,
+}
+
+
+def decode_traffic(workload_name: str):
+    import hashlib
+    h = hashlib.sha256()
+    for f in DECODE_TRAFFIC["sources"]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest() != DECODE_TRAFFIC["sha256"] or workload_name != DECODE_TRAFFIC["workload"]:
+        return None
+    return DECODE_TRAFFIC["fetch_bytes"] + DECODE_TRAFFIC["write_bytes"]
+
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -297,7 +322,8 @@ def main():
                      "decode_calls_total": float(dec_loop_ms.mean()), "answer_ppl": float(ppl_ms.mean())},
         "roofline": {"kernel": "reco_decode_attn (decode_split_kernel + decode_merge_kernel)", "bound": "hbm",
                      "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
-                     "traffic": None, "algorithmic_bytes_per_launch": dec_bytes_mean},
+                     "traffic": decode_traffic(wl.name), "traffic_unit": "bytes per decode_split_kernel launch",
+                     "algorithmic_bytes_per_launch": dec_bytes_mean},
     }
     if args.cpu_baseline:
         log("timing the CPU oracle on a bounded sample")

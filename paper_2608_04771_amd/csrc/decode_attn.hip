@@ -334,7 +334,8 @@ __global__ __launch_bounds__(kWave) void decode_merge_kernel(DecodeParams p) {
   const int S = p.splits;
   const bool append = p.k_new != nullptr && qi == 0;
 
-  // Query head 0 of the unit also commits the append: fetch the row now.
+  // Query head 0 of the unit also commits the append: fetch len and the row now.
+  const int len_in = qi == 0 ? p.len[cunit] : 0;
   T krow[kPer], vrow[kPer];
   if (append) {
     const T *ksrc = reinterpret_cast<const T *>(p.k_new) + qunit * D;
@@ -346,6 +347,17 @@ __global__ __launch_bounds__(kWave) void decode_merge_kernel(DecodeParams p) {
     }
   }
   const float *pml = p.part_ml + static_cast<size_t>(unit) * S * 32;
+  const float *po = p.part_o + (static_cast<size_t>(unit) * S * 16 + qi) * D;
+  // The first kPre splits' output slices are requested together with the
+  // statistics, so a call with at most kPre splits costs one memory round trip.
+  constexpr int kPre = 4;
+  float pre[kPre][kPer];
+#pragma unroll
+  for (int s = 0; s < kPre; ++s) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i)
+      pre[s][i] = s < S ? po[static_cast<size_t>(s) * 16 * D + lane + i * kWave] : 0.f;
+  }
   // Lane s holds split s's statistics, lane s - 64 the rest (S <= kMaxSplits = 128).
   const float m0 = lane < S ? pml[lane * 32 + qi] : -INFINITY;
   const float l0 = lane < S ? pml[lane * 32 + 16 + qi] : 0.f;
@@ -358,11 +370,16 @@ __global__ __launch_bounds__(kWave) void decode_merge_kernel(DecodeParams p) {
   const float w0 = (M != -INFINITY) ? fast_exp2(m0 - M) * inv : 0.f;
   const float w1 = (M != -INFINITY) ? fast_exp2(m1 - M) * inv : 0.f;
 
-  const float *po = p.part_o + (static_cast<size_t>(unit) * S * 16 + qi) * D;
   float acc[kPer];
 #pragma unroll
   for (int i = 0; i < kPer; ++i) acc[i] = 0.f;
-  for (int s = 0; s < S; ++s) {
+#pragma unroll
+  for (int s = 0; s < kPre; ++s) {
+    const float wgt = __shfl(w0, s, kWave);       // 0 for s >= S
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) acc[i] += wgt * pre[s][i];
+  }
+  for (int s = kPre; s < S; ++s) {
     const float wgt = __shfl(s < kWave ? w0 : w1, s & (kWave - 1), kWave);
 #pragma unroll
     for (int i = 0; i < kPer; ++i) acc[i] += wgt * po[static_cast<size_t>(s) * 16 * D + lane + i * kWave];
@@ -375,7 +392,6 @@ __global__ __launch_bounds__(kWave) void decode_merge_kernel(DecodeParams p) {
         L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
 
   if (qi != 0) return;
-  const int len_in = p.len[cunit];
   if (lane == 0 && (len_in < 0 || len_in > p.cap)) report(p.dev_err, 5 /*RECO_DEV_BAD_LENGTH*/);
   if (!append || len_in < 0 || len_in > p.cap) return;
   if (len_in == p.cap) {

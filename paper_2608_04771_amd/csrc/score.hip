@@ -4,15 +4,22 @@
 // (query head of h's group, window position) pairs.  Row r = g * w + t is the
 // query of head h*G + g at absolute position pos = L - w + t.  Three kernels:
 //   1. score_stats: per (unit, 512-key chunk), the fp32 running (max, sum of
-//      exp) of every window row over the chunk's keys (log2 domain);
+//      exp) of every window row over the chunk's keys (log2 domain), with
+//      S^T = K.Q^T so that a lane holds four keys of one row;
 //   2. score_rowmerge: per (unit, row), merge the chunk statistics into the
 //      row's softmax normaliser (max, 1/sum);
-//   3. score_mass: per (unit, chunk), recompute the logits and add
-//      exp2(x - max) / sum over all rows of each key; the four waves' column
-//      sums meet in LDS, so each score is written once, deterministically.
+//   3. score_mass: per (unit, chunk), recompute the logits as S = Q.K^T (a
+//      lane holds four rows of one key, summed in registers) and add
+//      exp2(x - max) / sum over all rows of each key; the waves' column sums
+//      meet in LDS, so each score is written once, deterministically.
 // Logits are S^T = K . Q^T on the matrix cores (16 keys x 16 rows per MFMA,
 // bf16 products accumulated in fp32); each wave owns a slice of row tiles
 // whose Q fragments stay in registers while the chunk's keys stream past.
+// The workgroup reads each 32-key block of K once, with coalesced
+// non-temporal loads (prefetched one block ahead), into a double-buffered
+// LDS stage that all its waves read in the MFMA operand layout.  Blocks
+// that every window row sees in full take a mask-free path; only the blocks
+// that reach into the window or past the end of the cache test each key.
 #include "reco_device.hpp"
 #include "reco_kernels.hpp"
 
@@ -23,8 +30,8 @@ namespace reco {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kWaves = 4;
-constexpr int kKeyTile = 16;
+constexpr int kWaves = 4;       // waves per scoring workgroup
+constexpr int kBlock = 32;        // keys per LDS block (two 16-key MFMA tiles)
 
 struct UnitInfo {
   int lc, b, h;
@@ -46,12 +53,24 @@ __device__ __forceinline__ UnitInfo unit_info(const ScoreParams &p, int unit) {
   return u;
 }
 
+template <typename T, int D>
+struct ScoreCfg {
+  using MF = Mfma<T>;
+  static constexpr int dq = D / 4;                       // head-dim elements per lane group
+  static constexpr int steps = dq / MF::kPerLane;        // MFMAs per 16x16 logit tile
+  static constexpr int row_bytes = D * (int)sizeof(T);
+  static constexpr int k_stride = row_bytes + 16;        // padded, 16-byte aligned LDS pitch
+  static constexpr int stage_bytes = kBlock * k_stride;
+  static constexpr int lanes_per_row = row_bytes / 16;
+  static constexpr int pieces = kBlock * lanes_per_row;              // 16-byte pieces per block
+  static constexpr int max_loads = pieces / (kWaves * kWave);        // per thread (4-wave workgroups)
+};
+
 template <typename T, int D, int RTW>
 struct RowBlock {
   using MF = Mfma<T>;
   using frag = typename MF::frag;
-  static constexpr int dq = D / 4;
-  static constexpr int steps = dq / MF::kPerLane;
+  static constexpr int steps = ScoreCfg<T, D>::steps;
   frag q[RTW][steps];
   int pos[RTW];      // absolute position of the lane's row (for causality)
   bool valid[RTW];   // the lane's row exists
@@ -68,7 +87,7 @@ struct RowBlock {
       pos[k] = ps;
       const T *qrow = reinterpret_cast<const T *>(p.q_win) +
                       (((static_cast<size_t>(u.lc) * p.batch + u.b) * p.hq + u.h * p.group + (valid[k] ? g : 0)) * p.w +
-                       (valid[k] ? t : 0)) * D + grp * dq;
+                       (valid[k] ? t : 0)) * D + grp * ScoreCfg<T, D>::dq;
 #pragma unroll
       for (int c = 0; c < steps; ++c)
         q[k][c] = valid[k] ? load_frag(qrow + c * MF::kPerLane) : zero_frag(frag{});
@@ -76,19 +95,97 @@ struct RowBlock {
   }
 };
 
+// The thread's 16-byte pieces of one 32-key block of K (piece i * 256 + thread).
 template <typename T, int D>
-__device__ __forceinline__ void load_key_tile(const T *kbase, int kb, int L, int col, int grp,
-                                              typename Mfma<T>::frag (&kf)[D / 4 / Mfma<T>::kPerLane]) {
-  const int key = kb + col;
-  const T *row = kbase + static_cast<size_t>(key < L ? key : 0) * D + grp * (D / 4);
+struct BlockRegs {
+  uint4 r[ScoreCfg<T, D>::max_loads];
+};
+
+// Global -> registers: the thread's pieces of the 32-key block at kb (rows
+// past the end of the cache read row 0 and are masked later).
+template <typename T, int D>
+__device__ __forceinline__ void load_block(BlockRegs<T, D> &regs, const T *kbase, int kb, int L) {
+  using Cfg = ScoreCfg<T, D>;
 #pragma unroll
-  for (int c = 0; c < D / 4 / Mfma<T>::kPerLane; ++c) kf[c] = load_frag(row + c * Mfma<T>::kPerLane);
+  for (int i = 0; i < Cfg::max_loads; ++i) {
+    const int piece = i * kThreads + static_cast<int>(threadIdx.x);
+    const int r = piece / Cfg::lanes_per_row;
+    const int key = kb + r;
+    const unsigned char *src =
+        reinterpret_cast<const unsigned char *>(kbase + static_cast<size_t>(key < L ? key : 0) * D);
+    regs.r[i] = nt_load_u4(src + (piece % Cfg::lanes_per_row) * 16);
+  }
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void store_block(unsigned char *stage, const BlockRegs<T, D> &regs) {
+  using Cfg = ScoreCfg<T, D>;
+#pragma unroll
+  for (int i = 0; i < Cfg::max_loads; ++i) {
+    const int piece = i * kThreads + static_cast<int>(threadIdx.x);
+    const int r = piece / Cfg::lanes_per_row;
+    *reinterpret_cast<uint4 *>(stage + r * Cfg::k_stride + (piece % Cfg::lanes_per_row) * 16) = regs.r[i];
+  }
+}
+
+// MFMA operand of 16-key tile kt of the staged block: lane holds key
+// kt*16 + col, head-dim slice grp*dq + c*kpl.
+template <typename T, int D>
+__device__ __forceinline__ void key_frags(const unsigned char *stage, int kt, int col, int grp,
+                                          typename Mfma<T>::frag (&kf)[ScoreCfg<T, D>::steps]) {
+  using Cfg = ScoreCfg<T, D>;
+  const T *row = reinterpret_cast<const T *>(stage + (kt * 16 + col) * Cfg::k_stride) + grp * Cfg::dq;
+#pragma unroll
+  for (int c = 0; c < Cfg::steps; ++c) kf[c] = load_frag(row + c * Mfma<T>::kPerLane);
+}
+
+// Statistics pass body for one 32-key block (two 16-key tiles): S^T = K.Q^T,
+// lane holds keys kb + kt*16 + 4*grp + i of row (tile0 + k)*16 + col; online
+// (max, sum) per lane, merged over the lane groups at the end of the chunk.
+template <typename T, int D, int RTW, bool FULL>
+__device__ __forceinline__ void stats_block(const ScoreParams &p, const UnitInfo &u, const RowBlock<T, D, RTW> &rb,
+                                            const unsigned char *stage, int kb, int col, int grp,
+                                            float (&m)[RTW], float (&z)[RTW]) {
+  using MF = Mfma<T>;
+  using Cfg = ScoreCfg<T, D>;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+    typename MF::frag kf[Cfg::steps];
+    key_frags<T, D>(stage, kt, col, grp, kf);
+#pragma unroll
+    for (int k = 0; k < RTW; ++k) {
+      f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < Cfg::steps; ++c) s = MF::mma(kf[c], rb.q[k][c], s);
+      float x[4];
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        x[i] = s[i] * p.scale_log2;
+        if constexpr (!FULL) {
+          const int key = kb + kt * 16 + 4 * grp + i;
+          x[i] = (key < u.L && (!p.causal || key <= rb.pos[k])) ? x[i] : -INFINITY;
+        }
+        tmax = fmaxf(tmax, x[i]);
+      }
+      const float mn = fmaxf(m[k], tmax);
+      if (FULL || mn != -INFINITY) {
+        float sum = z[k] * fast_exp2(m[k] - mn);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sum += fast_exp2(x[i] - mn);
+        z[k] = sum;
+        m[k] = mn;
+      }
+    }
+  }
 }
 
 template <typename T, int D, int RTW>
 __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreParams p) {
-  using MF = Mfma<T>;
+  constexpr int n_waves = kWaves;
+  using Cfg = ScoreCfg<T, D>;
   using RB = RowBlock<T, D, RTW>;
+  __shared__ __attribute__((aligned(16))) unsigned char stage[2][Cfg::stage_bytes];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int col = lane & 15, grp = lane >> 4;
@@ -99,9 +196,11 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreParams p) {
   const int k1 = min(u.L, k0 + kScoreChunk);
   const T *kbase = reinterpret_cast<const T *>(p.k) + u.cunit * p.cap * D;
   const int row_tiles = p.rows_pad / 16;
+  // Keys every valid window row sees: below L, and (causal) up to L - w.
+  const int full_end = p.causal ? min(u.L, u.L - p.w + 1) : u.L;
 
-  for (int tg = 0; tg < row_tiles; tg += kWaves * RTW) {
-    const int tile0 = tg + wave * RTW;
+  for (int tg = 0; tg < row_tiles; tg += n_waves * RTW) {
+    const int tile0 = tg + wave * RTW;   // tiles past row_tiles hold zero queries; never stored
     RB rb;
     rb.load(p, u, tile0, col, grp);
     float m[RTW], z[RTW];
@@ -110,42 +209,26 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreParams p) {
       m[k] = -INFINITY;
       z[k] = 0.f;
     }
-    for (int kb = k0; kb < k1; kb += kKeyTile) {
-      typename MF::frag kf[RB::steps];
-      load_key_tile<T, D>(kbase, kb, u.L, col, grp, kf);
-#pragma unroll
-      for (int k = 0; k < RTW; ++k) {
-        if (tile0 + k >= row_tiles) break;
-        f32x4_t s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < RB::steps; ++c) s = MF::mma(kf[c], rb.q[k][c], s);
-        float x[4];
-        float tmax = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = kb + 4 * grp + i;
-          const bool vis = key < u.L && (!p.causal || key <= rb.pos[k]);
-          x[i] = vis ? s[i] * p.scale_log2 : -INFINITY;
-          tmax = fmaxf(tmax, x[i]);
-        }
-        const float mn = fmaxf(m[k], tmax);
-        if (mn != -INFINITY) {
-          float acc = z[k] * fast_exp2(m[k] - mn);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) acc += fast_exp2(x[i] - mn);
-          z[k] = acc;
-          m[k] = mn;
-        }
-      }
+    BlockRegs<T, D> regs;
+    load_block<T, D>(regs, kbase, k0, u.L);
+    int buf = 0;
+    for (int kb = k0; kb < k1; kb += kBlock, buf ^= 1) {
+      store_block<T, D>(stage[buf], regs);
+      __syncthreads();   // block kb staged; every wave is done with the other buffer
+      if (kb + kBlock < k1) load_block<T, D>(regs, kbase, kb + kBlock, u.L);
+      if (kb + kBlock <= full_end)
+        stats_block<T, D, RTW, true>(p, u, rb, stage[buf], kb, col, grp, m, z);
+      else
+        stats_block<T, D, RTW, false>(p, u, rb, stage[buf], kb, col, grp, m, z);
     }
+    __syncthreads();   // the stage is reused by the next row-tile group
     // Merge the four lane groups that hold the same row, then store.
 #pragma unroll
     for (int k = 0; k < RTW; ++k) {
-      if (tile0 + k >= row_tiles) break;
       const float M = group4_max(m[k]);
       const float zz = (m[k] == -INFINITY) ? 0.f : z[k] * fast_exp2(m[k] - M);
       const float Z = group4_sum(zz);
-      if (grp == 0) {
+      if (grp == 0 && tile0 + k < row_tiles) {
         const int r = (tile0 + k) * 16 + col;
         float *dst = p.row_part + ((u.ounit * p.chunks + chunk) * p.rows_pad + r) * 2;
         dst[0] = M;
@@ -155,29 +238,49 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreParams p) {
   }
 }
 
-__global__ __launch_bounds__(kThreads) void score_rowmerge_kernel(ScoreParams p) {
-  const UnitInfo u = unit_info(p, blockIdx.y);
-  const int r = blockIdx.x * kThreads + threadIdx.x;
-  if (r >= p.rows_pad) return;
-  const int active = (u.L + kScoreChunk - 1) / kScoreChunk;
-  float M = -INFINITY;
-  for (int c = 0; c < active; ++c) M = fmaxf(M, p.row_part[((u.ounit * p.chunks + c) * p.rows_pad + r) * 2]);
-  double Z = 0.0;
-  if (M != -INFINITY) {
-    for (int c = 0; c < active; ++c) {
-      const float *src = p.row_part + ((u.ounit * p.chunks + c) * p.rows_pad + r) * 2;
-      if (src[0] != -INFINITY) Z += static_cast<double>(src[1]) * static_cast<double>(fast_exp2(src[0] - M));
+// Mass pass body for one 32-key block: S = Q.K^T, lane holds rows
+// (tile0 + k)*16 + 4*grp + i of key kb + kt*16 + col, so the lane sums its
+// rows in registers and only the four lane groups meet at the end.
+template <typename T, int D, int RTW, bool FULL>
+__device__ __forceinline__ void mass_block(const ScoreParams &p, const UnitInfo &u, const RowBlock<T, D, RTW> &rb,
+                                           const unsigned char *stage, int kb, int tile0, int col, int grp,
+                                           const float (&rmax)[RTW][4], const float (&rinv)[RTW][4],
+                                           float (&acc)[2]) {
+  using MF = Mfma<T>;
+  using Cfg = ScoreCfg<T, D>;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+    typename MF::frag kf[Cfg::steps];
+    key_frags<T, D>(stage, kt, col, grp, kf);
+    const int key = kb + kt * 16 + col;
+#pragma unroll
+    for (int k = 0; k < RTW; ++k) {
+      f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < Cfg::steps; ++c) s = MF::mma(rb.q[k][c], kf[c], s);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // Absent rows carry max = +inf and 1/sum = 0, so they add exactly 0.
+        const float e = fast_exp2(fmaf(s[i], p.scale_log2, -rmax[k][i]));
+        if constexpr (FULL) {
+          acc[kt] = fmaf(e, rinv[k][i], acc[kt]);
+        } else {
+          const int r = (tile0 + k) * 16 + 4 * grp + i;
+          const int pos = u.L - p.w + r % p.w;
+          const bool vis = key < u.L && (!p.causal || key <= pos);
+          acc[kt] += vis ? e * rinv[k][i] : 0.f;
+        }
+      }
     }
   }
-  float *dst = p.row_stat + (u.ounit * p.rows_pad + r) * 2;
-  dst[0] = (M == -INFINITY) ? 0.f : M;
-  dst[1] = (Z > 0.0) ? static_cast<float>(1.0 / Z) : 0.f;
 }
 
 template <typename T, int D, int RTW>
 __global__ __launch_bounds__(kThreads) void score_mass_kernel(ScoreParams p) {
-  using MF = Mfma<T>;
+  constexpr int n_waves = kWaves;
+  using Cfg = ScoreCfg<T, D>;
   using RB = RowBlock<T, D, RTW>;
+  __shared__ __attribute__((aligned(16))) unsigned char stage[2][Cfg::stage_bytes];
   __shared__ float part[kWaves][kScoreChunk];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
@@ -189,79 +292,112 @@ __global__ __launch_bounds__(kThreads) void score_mass_kernel(ScoreParams p) {
   const int k1 = min(u.L, k0 + kScoreChunk);
   const T *kbase = reinterpret_cast<const T *>(p.k) + u.cunit * p.cap * D;
   const int row_tiles = p.rows_pad / 16;
+  const int full_end = p.causal ? min(u.L, u.L - p.w + 1) : u.L;
 
-  for (int i = threadIdx.x; i < kWaves * kScoreChunk; i += kThreads) (&part[0][0])[i] = 0.f;
-  __syncthreads();
+  for (int i = threadIdx.x; i < n_waves * kScoreChunk; i += kThreads) (&part[0][0])[i] = 0.f;
 
-  for (int tg = 0; tg < row_tiles; tg += kWaves * RTW) {
+  for (int tg = 0; tg < row_tiles; tg += n_waves * RTW) {
     const int tile0 = tg + wave * RTW;
     RB rb;
     rb.load(p, u, tile0, col, grp);
-    float rmax[RTW], rinv[RTW];
+    // Normalisers of the lane's rows (tile0 + k)*16 + 4*grp + i.
+    float rmax[RTW][4], rinv[RTW][4];
 #pragma unroll
     for (int k = 0; k < RTW; ++k) {
-      const int r = (tile0 + k) * 16 + col;
-      const bool in = (tile0 + k) < row_tiles;
-      const float *st = p.row_stat + (u.ounit * p.rows_pad + (in ? r : 0)) * 2;
-      rmax[k] = in ? st[0] : 0.f;
-      rinv[k] = in ? st[1] : 0.f;
-      rb.valid[k] = rb.valid[k] && in;
-    }
-    for (int kb = k0; kb < k1; kb += kKeyTile) {
-      typename MF::frag kf[RB::steps];
-      load_key_tile<T, D>(kbase, kb, u.L, col, grp, kf);
-      float acc[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int k = 0; k < RTW; ++k) {
-        if (tile0 + k >= row_tiles) break;
-        f32x4_t s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < RB::steps; ++c) s = MF::mma(kf[c], rb.q[k][c], s);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = kb + 4 * grp + i;
-          const bool vis = rb.valid[k] && key < u.L && (!p.causal || key <= rb.pos[k]);
-          const float e = fast_exp2(s[i] * p.scale_log2 - rmax[k]) * rinv[k];
-          acc[i] += vis ? e : 0.f;
-        }
-      }
-      // Sum over the 16 rows of each tile (lanes of one group), then bank the key sums.
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float tot = row16_sum(acc[i]);
-        if (col == 0) part[wave][kb - k0 + 4 * grp + i] += tot;
+        const int r = (tile0 + k) * 16 + 4 * grp + i;
+        const bool in = (tile0 + k) < row_tiles;
+        const float *st = p.row_stat + (u.ounit * p.rows_pad + (in ? r : 0)) * 2;
+        rmax[k][i] = in ? st[0] : INFINITY;
+        rinv[k][i] = in ? st[1] : 0.f;
       }
     }
+    BlockRegs<T, D> regs;
+    load_block<T, D>(regs, kbase, k0, u.L);
+    int buf = 0;
+    for (int kb = k0; kb < k1; kb += kBlock, buf ^= 1) {
+      store_block<T, D>(stage[buf], regs);
+      __syncthreads();   // block kb staged; every wave is done with the other buffer
+      if (kb + kBlock < k1) load_block<T, D>(regs, kbase, kb + kBlock, u.L);
+      float acc[2] = {0.f, 0.f};
+      if (kb + kBlock <= full_end)
+        mass_block<T, D, RTW, true>(p, u, rb, stage[buf], kb, tile0, col, grp, rmax, rinv, acc);
+      else
+        mass_block<T, D, RTW, false>(p, u, rb, stage[buf], kb, tile0, col, grp, rmax, rinv, acc);
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const float tot = group4_sum(acc[kt]);
+        if (grp == 0) part[wave][kb - k0 + kt * 16 + col] += tot;
+      }
+    }
+    __syncthreads();   // the stage is reused by the next row-tile group
   }
   __syncthreads();
   float *out = p.scores + u.ounit * p.cap;
   for (int j = threadIdx.x; j < k1 - k0; j += kThreads) {
     float s = 0.f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) s += part[w][j];
+    for (int w = 0; w < n_waves; ++w) s += part[w][j];
     out[k0 + j] = s;
   }
 }
 
+// Row normalisers: (max, 1/sum) of every valid window row; absent rows get
+// (+inf, 0) so that the mass pass adds exactly zero for them.
+__global__ __launch_bounds__(kThreads) void score_rowmerge_kernel(ScoreParams p) {
+  const UnitInfo u = unit_info(p, blockIdx.y);
+  const int r = blockIdx.x * kThreads + threadIdx.x;
+  if (r >= p.rows_pad) return;
+  const int t = r % p.w;
+  const bool valid = r < p.rows && u.L - p.w + t >= 0;
+  const int active = (u.L + kScoreChunk - 1) / kScoreChunk;
+  float M = -INFINITY;
+  for (int c = 0; c < active; ++c) M = fmaxf(M, p.row_part[((u.ounit * p.chunks + c) * p.rows_pad + r) * 2]);
+  double Z = 0.0;
+  if (M != -INFINITY) {
+    for (int c = 0; c < active; ++c) {
+      const float *src = p.row_part + ((u.ounit * p.chunks + c) * p.rows_pad + r) * 2;
+      if (src[0] != -INFINITY) Z += static_cast<double>(src[1]) * static_cast<double>(fast_exp2(src[0] - M));
+    }
+  }
+  float *dst = p.row_stat + (u.ounit * p.rows_pad + r) * 2;
+  const bool ok = valid && M != -INFINITY && Z > 0.0;
+  dst[0] = ok ? M : INFINITY;
+  dst[1] = ok ? static_cast<float>(1.0 / Z) : 0.f;
+}
+
 template <typename T, int D, int RTW>
-hipError_t launch_rtw(const ScoreParams &p, hipStream_t s) {
+hipError_t launch_rtw(const ScoreParams &p, int waves, hipStream_t s) {
   const int units = p.n_layers * p.batch * p.hkv;
-  hipLaunchKernelGGL((score_stats_kernel<T, D, RTW>), dim3(p.chunks, units), dim3(kThreads), 0, s, p);
+  hipLaunchKernelGGL((score_stats_kernel<T, D, RTW>), dim3(p.chunks, units), dim3(waves * kWave), 0, s, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(score_rowmerge_kernel, dim3((p.rows_pad + kThreads - 1) / kThreads, units), dim3(kThreads), 0, s, p);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((score_mass_kernel<T, D, RTW>), dim3(p.chunks, units), dim3(kThreads), 0, s, p);
+  hipLaunchKernelGGL((score_mass_kernel<T, D, RTW>), dim3(p.chunks, units), dim3(waves * kWave), 0, s, p);
   return hipGetLastError();
 }
 
+// Row tiles per wave: the four waves split the G * w window rows evenly, up
+// to eight 16-row tiles each (more rows loop over groups of 32 tiles).  Each
+// staged K fragment then feeds up to eight MFMA tiles; spreading the rows
+// over more waves (4 tiles each) measured 1.4x slower on the 7B window
+// (448 rows) despite the higher occupancy.
 template <typename T, int D>
 hipError_t launch_typed(const ScoreParams &p, hipStream_t s) {
   const int row_tiles = p.rows_pad / 16;
-  if (row_tiles <= kWaves * 2) return launch_rtw<T, D, 2>(p, s);
-  if (row_tiles <= kWaves * 4) return launch_rtw<T, D, 4>(p, s);
-  return launch_rtw<T, D, 8>(p, s);
+  switch ((row_tiles + kWaves - 1) / kWaves) {
+    case 1: return launch_rtw<T, D, 1>(p, kWaves, s);
+    case 2: return launch_rtw<T, D, 2>(p, kWaves, s);
+    case 3: return launch_rtw<T, D, 3>(p, kWaves, s);
+    case 4: return launch_rtw<T, D, 4>(p, kWaves, s);
+    case 5: return launch_rtw<T, D, 5>(p, kWaves, s);
+    case 6: return launch_rtw<T, D, 6>(p, kWaves, s);
+    case 7: return launch_rtw<T, D, 7>(p, kWaves, s);
+    default: return launch_rtw<T, D, 8>(p, kWaves, s);
+  }
 }
 
 }  // namespace

@@ -45,9 +45,9 @@ ANSWER_LEN = 32
 DECODE_TRAFFIC = {
     "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
                 "paper_2608_04771_amd/csrc/reco_kernels.hpp"),
-    "sha256": "52af6de82fb9a3abb109ebb45eb7b605b98a1f001936a12147e55d3b24044f39",
+    "sha256": "a1b36a34efb9a4fe6fb3ae4e6d2b1f2e2eab9cccff3e0aebc2017ee2acc00685",
     "workload": "7b-28L-28q4kv-d128-bf16-L16384",
-    "fetch_bytes": 555355048,
+    "fetch_bytes": 555420213,
     "write_bytes": 817152,
 }
 

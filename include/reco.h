@@ -200,6 +200,12 @@ reco_status_t reco_answer_ppl(const float *logits, const int32_t *tokens, int32_
 double reco_retention_from_reward(double v, double lo, double hi);
 double reco_retention_eq1(const double *v_hist, int32_t n, double lambda, double delta);
 
+/* [host] The kept count of Section 3.2 that reco_select_compact uses:
+ * m = min(L, max(min(w, L), ceil(r * L))) with r * L an IEEE fp64 product;
+ * -1 when r is not in (0, 1], L < 0 or w < 1.  Lets a host controller track
+ * cache lengths without reading them back from the device. */
+int32_t reco_kept_count(int32_t L, int32_t w, double r);
+
 /* [host] Human-readable status and the ABI version (RECO_ABI_VERSION). */
 const char *reco_status_str(reco_status_t status);
 int32_t reco_abi_version(void);

@@ -33,7 +33,7 @@ EXPORTED = [
     "reco_score_workspace_size", "reco_score", "reco_select_compact_workspace_size", "reco_select_compact",
     "reco_decode_attn_workspace_size", "reco_decode_attn", "reco_logit_penalty",
     "reco_answer_ppl_workspace_size", "reco_answer_ppl", "reco_retention_from_reward", "reco_retention_eq1",
-    "reco_status_str", "reco_abi_version",
+    "reco_kept_count", "reco_status_str", "reco_abi_version",
 ]
 
 
@@ -69,6 +69,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "reco_answer_ppl": (I32, [P, P, I32, I32, I32, F32, P, P, P, SZ, P, P]),
         "reco_retention_from_reward": (F64, [F64, F64, F64]),
         "reco_retention_eq1": (F64, [ctypes.POINTER(ctypes.c_double), I32, F64, F64]),
+        "reco_kept_count": (I32, [I32, I32, F64]),
         "reco_status_str": (ctypes.c_char_p, [I32]),
         "reco_abi_version": (I32, []),
     }
@@ -278,6 +279,10 @@ def reco_retention_from_reward(v: float, lo: float = 0.3, hi: float = 1.0) -> fl
 def reco_retention_eq1(v_hist: Sequence[float], lam: float = 0.25, delta: float = 0.1) -> float:
     arr = (ctypes.c_double * len(v_hist))(*[float(x) for x in v_hist])
     return float(load_library().reco_retention_eq1(arr, len(v_hist), float(lam), float(delta)))
+
+
+def reco_kept_count(L: int, w: int, r: float) -> int:
+    return int(load_library().reco_kept_count(int(L), int(w), float(r)))
 
 
 def reco_abi_version() -> int:

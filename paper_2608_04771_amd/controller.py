@@ -1,0 +1,180 @@
+"""Host control plane of reward-coordinated decoding (Section 3), on the HIP kernels.
+
+The paper's loop, per completed reasoning step i with process reward v_i:
+
+* reward-driven retention (Section 3.2, Eq. 1): once the cache has grown by
+  S tokens since the last compression, compress it to m_i = lambda_i * L
+  tokens, lambda_i set by the step's reward relative to the trajectory's own
+  reward statistics (or by the fixed map r = clamp(1 - v/2, 0.3, 1));
+* attention-guided selection (Eq. 2) over the w most recent queries;
+* the reward band of the just-completed step sets the reflection-token
+  penalty applied to every logit row of the next step (Eq. 3-4);
+* two consecutive top-band rewards trigger the answer probe, whose
+  perplexity decides the stop (Eq. 5-6).
+
+`RewardSchedule` holds the pure host bookkeeping (reward history, retention,
+compression trigger, probe trigger) and runs without a GPU.  `RecoDecoder`
+drives the kernels through the binding: it keeps the window queries in a ring
+buffer on the device, calls reco_decode_attn / reco_logit_penalty per token
+and reco_score / reco_select_compact at step boundaries.  All arithmetic of
+the method runs in the library; this module decides when, and moves data.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Optional, Sequence
+
+import torch
+
+from . import binding as B
+
+
+@dataclasses.dataclass
+class RecoPolicy:
+    """Hyper-parameters of the loop.  Defaults are the fixed set of Section 4.1
+    (lambda = 0.25, delta = 0.1, w = 32, tau_l = 0.4, tau_h = 0.8, tau_p = 1.1);
+    `retention="clamp"` selects r = clamp(1 - v/2, lo, hi) instead of Eq. 1."""
+    retention: str = "eq1"           # "eq1" | "clamp"
+    lam: float = 0.25
+    delta: float = 0.1
+    lo: float = 0.3
+    hi: float = 1.0
+    window: int = 32
+    interval: int = 0                # S: compress once the cache grew by S tokens (0: every step boundary)
+    tau_lo: float = 0.4
+    tau_hi: float = 0.8
+    tau_p: float = 1.1
+    betas: Sequence[float] = (0.0, 1.0, 3.0)   # penalty in the low / middle / high band
+
+
+class RewardSchedule:
+    """Per-sequence host state: reward history, cache length bookkeeping and
+    the two triggers.  Lengths follow the same fp64 kept-count rule as the
+    select kernel, so no device read-back is needed."""
+
+    def __init__(self, policy: RecoPolicy, prompt_len: int):
+        self.policy = policy
+        self.rewards: List[float] = []
+        self.length = int(prompt_len)          # L: current cache length
+        self.length_at_compress = int(prompt_len)   # L_{i-1} (the prompt length at first)
+        self.top_streak = 0
+
+    def retention(self) -> float:
+        p = self.policy
+        v = self.rewards[-1]
+        if p.retention == "clamp":
+            return B.reco_retention_from_reward(v, p.lo, p.hi)
+        return B.reco_retention_eq1(self.rewards, p.lam, p.delta)
+
+    def token_appended(self, n: int = 1):
+        self.length += n
+
+    def end_step(self, reward: float):
+        """Record v_i.  Returns (compress, r, probe): whether the cache is due
+        for compression (grown by >= S since the last one), the retention to
+        use, and whether the answer probe is due (v >= tau_h twice in a row)."""
+        self.rewards.append(float(reward))
+        p = self.policy
+        self.top_streak = self.top_streak + 1 if reward >= p.tau_hi else 0
+        probe = self.top_streak >= 2
+        compress = self.length - self.length_at_compress >= max(1, p.interval)
+        r = self.retention()
+        return compress, r, probe
+
+    def compressed(self, r: float):
+        self.length = B.reco_kept_count(self.length, self.policy.window, r)
+        self.length_at_compress = self.length
+
+
+class RecoDecoder:
+    """Drives one batch of sequences through decode steps and step-boundary
+    compressions.  All sequences share step boundaries (one schedule per
+    sequence; their rewards may differ).
+
+    cache      : KVCache holding the prompt's K/V (length = prompt length)
+    n_q_heads  : query heads (GQA group = n_q_heads / n_kv_heads)
+    prompt_q   : [NL][B][Hq][w][D] queries of the last w prompt tokens
+    refl_ids   : int32 device tensor of reflection-token ids (the set R)
+    """
+
+    def __init__(self, cache: B.KVCache, n_q_heads: int, policy: RecoPolicy, prompt_q: torch.Tensor,
+                 refl_ids: Optional[torch.Tensor] = None, record_kept: bool = False):
+        NL, Bsz, H, Cap, D = cache.shape
+        w = policy.window
+        if tuple(prompt_q.shape) != (NL, Bsz, n_q_heads, w, D):
+            raise ValueError("prompt_q must be [NL][B][Hq][w][D]")
+        self.cache, self.policy, self.hq = cache, policy, n_q_heads
+        dev = cache.k.device
+        prompt_len = int(cache.length[0, 0, 0].item())
+        self.sched = [RewardSchedule(policy, prompt_len) for _ in range(Bsz)]
+        self.ring = prompt_q.clone()                      # row t % w holds the query of token t
+        self.count = prompt_len                           # tokens seen (absolute position of the next one)
+        self.refl = refl_ids
+        self.band_reward = torch.zeros(Bsz, dtype=torch.float32, device=dev)   # no penalty before the first reward
+        self.ws_dec = B.decode_workspace(cache, n_q_heads)
+        self.ws_score = torch.empty(B.score_workspace_size(cache, n_q_heads, w), dtype=torch.uint8, device=dev)
+        self.ws_sel = torch.empty(B.select_compact_workspace_size(cache), dtype=torch.uint8, device=dev)
+        self.scores = torch.zeros((NL, Bsz, H, Cap), dtype=torch.float32, device=dev)
+        self.kept = torch.zeros((NL, Bsz, H, Cap), dtype=torch.int32, device=dev) if record_kept else None
+        self.retention = torch.ones(Bsz, dtype=torch.float64, device=dev)
+        self.dev_err = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.out = torch.empty((NL, Bsz, n_q_heads, D), dtype=cache.k.dtype, device=dev)
+        self.lse = torch.empty((NL, Bsz, n_q_heads), dtype=torch.float32, device=dev)
+        # Positions 0..prompt_len-1 are in the cache; the ring's rows hold
+        # prompt positions prompt_len - w .. prompt_len - 1 in order, i.e. the
+        # row of position p is p % w once rotated into place.
+        shift = prompt_len % w
+        if shift:
+            self.ring = torch.roll(self.ring, shifts=shift, dims=3).contiguous()
+
+    def decode(self, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+               logits: Optional[torch.Tensor] = None):
+        """One generated token: store its query in the window ring, attend
+        (appending its K/V) and apply the current reflection penalty to its
+        logit rows ([B][vocab], in place).  Returns (out, lse)."""
+        w = self.policy.window
+        self.ring[:, :, :, self.count % w, :].copy_(q)
+        B.reco_decode_attn(self.cache, q, k_new, v_new, out=self.out, lse=self.lse, ws=self.ws_dec,
+                           dev_err=self.dev_err)
+        if logits is not None and self.refl is not None:
+            p = self.policy
+            B.reco_logit_penalty(logits, self.refl, self.band_reward, p.tau_lo, p.tau_hi, *p.betas,
+                                 dev_err=self.dev_err)
+        self.count += 1
+        for s in self.sched:
+            s.token_appended()
+        return self.out, self.lse
+
+    def window_queries(self) -> torch.Tensor:
+        """The last w queries in order (row t = position L - w + t)."""
+        w = self.policy.window
+        return torch.roll(self.ring, shifts=-(self.count % w), dims=3).contiguous()
+
+    def end_step(self, rewards: Sequence[float]):
+        """A reasoning step ended with process rewards v (one per sequence).
+        Compresses when due and updates the penalty band for the next step.
+        Returns (compressed, probe flags per sequence)."""
+        decisions = [s.end_step(v) for s, v in zip(self.sched, rewards)]
+        self.band_reward.copy_(torch.tensor([float(v) for v in rewards], dtype=torch.float32))
+        probe = [d[2] for d in decisions]
+        due = [d[0] for d in decisions]
+        if not any(due):
+            return False, probe
+        # Sequences not due keep everything (r = 1 keeps every row in place).
+        r = [d[1] if d[0] else 1.0 for d in decisions]
+        self.retention.copy_(torch.tensor(r, dtype=torch.float64))
+        B.reco_score(self.cache, self.window_queries(), self.policy.window, scores=self.scores, ws=self.ws_score,
+                     dev_err=self.dev_err)
+        B.reco_select_compact(self.cache, self.scores, self.retention, self.policy.window, kept_idx=self.kept,
+                              ws=self.ws_sel, dev_err=self.dev_err)
+        for s, d, rr in zip(self.sched, due, r):
+            if d:
+                s.compressed(rr)
+        return True, probe
+
+    def answer_ppl(self, logits: torch.Tensor, tokens: torch.Tensor):
+        """Eq. 5-6 on a probe answer: (ppl [B], stop [B])."""
+        return B.reco_answer_ppl(logits, tokens, self.policy.tau_p, dev_err=self.dev_err)
+
+    def lengths(self) -> List[int]:
+        return [s.length for s in self.sched]

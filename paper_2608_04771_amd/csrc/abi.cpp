@@ -77,6 +77,15 @@ double reco_retention_eq1(const double *v_hist, int32_t n, double lambda, double
   return lambda - delta * (v_hist[n - 1] - mean) / (vmax - vmin);
 }
 
+int32_t reco_kept_count(int32_t L, int32_t w, double r) {
+  if (!(r > 0.0 && r <= 1.0) || L < 0 || w < 1) return -1;
+  const int32_t w_eff = w < L ? w : L;
+  int32_t m = static_cast<int32_t>(ceil(r * static_cast<double>(L)));
+  if (m < w_eff) m = w_eff;
+  if (m > L) m = L;
+  return m;
+}
+
 // ---------------------------------------------------------------- score
 size_t reco_score_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers, int32_t n_q_heads, int32_t w) {
   if (!cache_ok(cache) || n_layers < 1 || w < 1) return 0;

@@ -49,6 +49,19 @@ def test_retention_policies_match_oracle():
     assert B.reco_retention_eq1([0.4, 0.4], 0.25, 0.1) == 0.25
 
 
+@pytest.mark.parametrize("L,w,r", [(2048, 32, 0.75), (16384, 64, 0.5807587504386902), (1001, 32, 0.75),
+                                   (7, 32, 0.5), (100, 1, 1.0), (0, 4, 0.5), (1, 1, 0.3)])
+def test_kept_count_matches_oracle(L, w, r):
+    assert B.reco_kept_count(L, w, r) == oracle.kept_count(L, w, r)
+
+
+def test_kept_count_rejects_bad_retention():
+    assert B.reco_kept_count(100, 8, 0.0) == -1
+    assert B.reco_kept_count(100, 8, 1.5) == -1
+    assert B.reco_kept_count(100, 8, float("nan")) == -1
+    assert B.reco_kept_count(-1, 8, 0.5) == -1
+
+
 def _fake_cache(**kw):
     d = dict(k=0x1000, v=0x2000, len=0x3000, n_layers=2, batch=1, n_kv_heads=2, capacity=64, head_dim=128,
              dtype=B.RECO_BF16)

@@ -30,7 +30,7 @@ import numpy as np
 import torch
 
 __all__ = ["Workload", "WORKLOADS", "CacheInputs", "make_cache", "make_decode_inputs",
-           "make_logits", "make_reflection_ids", "make_answer_tokens"]
+           "make_logits", "make_reflection_ids", "make_answer_tokens", "make_step_lengths", "make_rewards"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -87,6 +87,11 @@ WORKLOADS = {
     # rewards ~ Beta(2,2).
     "7b-batch32": Workload("7b-28L-28q4kv-d128-bf16-B32-L4k-32k", 28, 32, 28, 4, 128, "bf16",
                            (4096, 32768), 64, 256, "beta22", 1002, ragged=True, vocab=152064),
+    # 8B-shaped full trajectory: 32 layers, 32 query / 8 KV heads, a 512-token
+    # prompt, then up to 32,768 generated tokens in steps of Geometric(mean 200)
+    # length, rewards ~ Beta(2,5) at every step boundary, 128,256-token vocabulary.
+    "8b-trajectory": Workload("8b-32L-32q8kv-d128-bf16-prompt512-gen32768", 32, 1, 32, 8, 128, "bf16", (512,), 32,
+                              32768, "beta25", 1003, vocab=128256),
     # 32B-shaped: 64 layers, 40 query / 8 KV heads, batch 8, 65,536 cached tokens.
     "32b64k": Workload("32b-64L-40q8kv-d128-bf16-B8-L65536", 64, 8, 40, 8, 128, "bf16", (65536,), 32, 64,
                        "beta22", 1004, vocab=152064),
@@ -195,6 +200,30 @@ def make_logits(rows: int, vocab: int, seed: int, sigma: float = 3.0, device="cp
     g = _gen(seed, device)
     shp = (rows, vocab) if shape is None else tuple(shape)
     return sigma * torch.randn(shp, generator=g, device=device, dtype=torch.float32)
+
+
+def make_step_lengths(total: int, mean: float, seed: int) -> np.ndarray:
+    """Reasoning-step lengths ~ Geometric(1/mean) until `total` tokens."""
+    rng = np.random.default_rng(seed)
+    out, t = [], 0
+    while t < total:
+        n = int(rng.geometric(1.0 / mean))
+        n = min(n, total - t)
+        out.append(n)
+        t += n
+    return np.asarray(out, dtype=np.int64)
+
+
+def make_rewards(kind: str, n: int, batch: int, seed: int) -> np.ndarray:
+    """Process rewards [n][batch] ~ U(0,1), Beta(2,2) or Beta(2,5)."""
+    rng = np.random.default_rng(seed)
+    if kind == "uniform":
+        v = rng.uniform(0.0, 1.0, size=(n, batch))
+    elif kind == "beta22":
+        v = rng.beta(2.0, 2.0, size=(n, batch))
+    else:
+        v = rng.beta(2.0, 5.0, size=(n, batch))
+    return v.astype(np.float32)
 
 
 def make_reflection_ids(n: int, vocab: int, seed: int) -> np.ndarray:

@@ -24,7 +24,10 @@ design notes):
 * decode appends the new token's K/V row before attending to it;
 * reflection-penalty bands compare v in float32 exactly as Eq. 3 writes them
   (<=, strict middle band, >=); each distinct reflection id is penalised once;
-* answer perplexity uses natural logarithms and the raw logits.
+* answer perplexity uses natural logarithms and the raw logits;
+* sampling from softmax(z~ / T) is the Gumbel-max draw argmax(z~ / T + G)
+  (T = 0: plain argmax), lowest index on ties, with G from a Philox4x32-10
+  stream keyed by (seed, row, offset) -- the paper names no generator.
 """
 from __future__ import annotations
 
@@ -36,6 +39,7 @@ import numpy as np
 __all__ = [
     "retention_from_reward", "retention_eq1", "kept_count", "score_unit", "select_unit",
     "compact_unit", "decode_unit", "penalty_band", "logit_penalty", "answer_ppl",
+    "philox4x32_10", "uniform_from_bits", "gumbel_noise", "penalty_sample",
 ]
 
 
@@ -288,3 +292,72 @@ def decode_cache(K: np.ndarray, V: np.ndarray, lens: np.ndarray, Q: np.ndarray, 
             V[l, b, h, n] = vn
             lens[l, b, h] = n + 1
     return out, lse
+
+
+# ---------------------------------------------------------------------------
+# Penalised sampling (Section 3.3: sample from softmax of the penalised logits)
+# ---------------------------------------------------------------------------
+
+# Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy
+# as 1, 2, 3", SC 2011): multipliers and Weyl key increments of the paper.
+_PHILOX_M0, _PHILOX_M1 = 0xD2511F53, 0xCD9E8D57
+_PHILOX_W0, _PHILOX_W1 = 0x9E3779B9, 0xBB67AE85
+
+
+def philox4x32_10(counter, key):
+    """Philox4x32 with 10 rounds.  counter: four uint32 arrays (broadcast
+    together), key: two uint32 scalars.  Returns four uint32 arrays."""
+    mask = np.uint64(0xFFFFFFFF)
+    c = [np.asarray(x, dtype=np.uint64) for x in counter]
+    k0, k1 = np.uint64(key[0]), np.uint64(key[1])
+    for rnd in range(10):
+        p0 = np.uint64(_PHILOX_M0) * c[0]
+        p1 = np.uint64(_PHILOX_M1) * c[2]
+        hi0, lo0 = p0 >> np.uint64(32), p0 & mask
+        hi1, lo1 = p1 >> np.uint64(32), p1 & mask
+        c = [hi1 ^ c[1] ^ k0, lo1, hi0 ^ c[3] ^ k1, lo0]
+        if rnd < 9:
+            k0 = (k0 + np.uint64(_PHILOX_W0)) & mask
+            k1 = (k1 + np.uint64(_PHILOX_W1)) & mask
+    return [x.astype(np.uint32) for x in c]
+
+
+def uniform_from_bits(x: np.ndarray) -> np.ndarray:
+    """Open-interval uniform from 32 random bits, float32: the top 23 bits
+    pick one of 2^23 equal cells of (0, 1) and U is the cell's midpoint,
+    (k + 1/2) * 2^-23 with k = x >> 9.  Every midpoint is an exact float32
+    (2k + 1 < 2^24), so U never rounds to 0 or 1 and U(x) + U(~x) = 1."""
+    k = (np.asarray(x, dtype=np.uint32) >> np.uint32(9)).astype(np.float32)
+    return (k * np.float32(2.0 ** -23) + np.float32(2.0 ** -24)).astype(np.float32)
+
+
+def gumbel_noise(row: int, vocab: int, seed: int, offset: int) -> np.ndarray:
+    """Gumbel(0,1) noise of one logit row, float32: G_j = -log(-log(U_j)),
+    U_j = uniform_from_bits(x_j), x_j the (j % 4)-th output of Philox on
+    counter (j / 4, row, offset low, offset high), key (seed low, seed high)."""
+    j = np.arange(vocab, dtype=np.uint64)
+    blk = j // np.uint64(4)
+    outs = philox4x32_10([blk, np.full_like(blk, row), np.full_like(blk, offset & 0xFFFFFFFF),
+                          np.full_like(blk, (offset >> 32) & 0xFFFFFFFF)],
+                         (seed & 0xFFFFFFFF, (seed >> 32) & 0xFFFFFFFF))
+    x = np.choose((j % np.uint64(4)).astype(np.int64), outs).astype(np.uint32)
+    u = uniform_from_bits(x)
+    return (-np.log(-np.log(u))).astype(np.float32)
+
+
+def penalty_sample(z: np.ndarray, refl_ids, reward, tau_lo, tau_hi, beta_lo, beta_mid, beta_hi,
+                   temperature: float, seed: int, offset: int):
+    """Eq. 3-4 on every row, then the next token of each row from
+    softmax(z~ / T): argmax of z~ (T = 0, lowest index on ties) or the
+    Gumbel-max draw argmax(z~ / T + G).  Returns (penalised float32 rows,
+    tokens int64, the float32 values the argmax was taken over)."""
+    zp = logit_penalty(z, refl_ids, reward, tau_lo, tau_hi, beta_lo, beta_mid, beta_hi)
+    rows, vocab = zp.shape
+    vals = np.empty_like(zp)
+    for b in range(rows):
+        if temperature == 0:
+            vals[b] = zp[b]
+        else:
+            vals[b] = (zp[b] / np.float32(temperature)).astype(np.float32) + gumbel_noise(b, vocab, seed, offset)
+    tokens = np.argmax(vals, axis=1)           # first maximum: lowest index on ties
+    return zp, tokens.astype(np.int64), vals

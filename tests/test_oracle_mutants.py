@@ -12,8 +12,11 @@ import pytest
 import oracle
 import oracle.reco_oracle as ro
 import test_oracle_pins as pins
+import test_oracle_sampling as spins
 
 _ORIG_PPL = ro.answer_ppl
+_ORIG_GUMBEL = ro.gumbel_noise
+_ORIG_PENALTY = ro.logit_penalty
 
 
 # ----------------------------------------------------------------- mutants
@@ -215,6 +218,39 @@ def _ppl_sum(logits, tokens, tau_p):
     return ppl, ppl <= tau_p
 
 
+def _gumbel_sign_flipped(row, vocab, seed, offset):
+    return (-_ORIG_GUMBEL(row, vocab, seed, offset)).astype(np.float32)
+
+
+def _uniform_missing_half_cell(x):
+    # planted: U = k * 2^-23 without the half-cell offset, so U can be 0 and is biased low
+    k = (np.asarray(x, dtype=np.uint32) >> np.uint32(9)).astype(np.float32)
+    return (k * np.float32(2.0 ** -23)).astype(np.float32)
+
+
+def _uniform_24_bits(x):
+    # planted: a 24-bit grid, whose top midpoint 1 - 2^-25 rounds to 1.0 in float32
+    k = (np.asarray(x, dtype=np.uint32) >> np.uint32(8)).astype(np.float32)
+    return (k * np.float32(2.0 ** -24) + np.float32(2.0 ** -25)).astype(np.float32)
+
+
+def _sample_without_penalty(z, refl_ids, reward, tau_lo, tau_hi, b_lo, b_mid, b_hi, temperature, seed, offset):
+    zp = np.array(z, dtype=np.float32, copy=True)            # planted: penalty never applied
+    vals = zp if temperature == 0 else np.stack([zp[b] / np.float32(temperature) + _ORIG_GUMBEL(b, zp.shape[1], seed, offset)
+                                                 for b in range(zp.shape[0])])
+    return zp, np.argmax(vals, axis=1), vals
+
+
+def _sample_temperature_multiplied(z, refl_ids, reward, tau_lo, tau_hi, b_lo, b_mid, b_hi, temperature, seed, offset):
+    zp = _ORIG_PENALTY(z, refl_ids, reward, tau_lo, tau_hi, b_lo, b_mid, b_hi)
+    vals = zp if temperature == 0 else np.stack([zp[b] * np.float32(temperature) + _ORIG_GUMBEL(b, zp.shape[1], seed, offset)
+                                                 for b in range(zp.shape[0])])
+    return zp, np.argmax(vals, axis=1), vals
+
+
+SAMPLING_PINS = [spins.test_gumbel_noise_moments, spins.test_greedy_is_argmax_of_penalised_logits,
+                 spins.test_sampling_distribution_is_softmax_of_penalised_logits]
+
 CASES = (
     [("score_unit", name, fn, SCORE_PINS) for name, fn in SCORE_MUTANTS.items()]
     + [("select_unit", name, fn, SELECT_PINS) for name, fn in SELECT_MUTANTS.items()]
@@ -227,7 +263,13 @@ CASES = (
        ("answer_ppl", "log_base_two", _ppl_log2, [pins.test_ppl_uniform_logits_equals_vocab,
                                                   pins.test_ppl_equals_exp_cross_entropy]),
        ("answer_ppl", "sum_not_mean", _ppl_sum, [pins.test_ppl_uniform_logits_equals_vocab,
-                                                 pins.test_ppl_equals_exp_cross_entropy])]
+                                                 pins.test_ppl_equals_exp_cross_entropy]),
+       ("gumbel_noise", "sign_flipped", _gumbel_sign_flipped, SAMPLING_PINS),
+       ("uniform_from_bits", "missing_half_cell", _uniform_missing_half_cell,
+        [spins.test_uniform_grid_is_open_and_symmetric]),
+       ("uniform_from_bits", "grid_of_24_bits", _uniform_24_bits, [spins.test_uniform_grid_is_open_and_symmetric]),
+       ("penalty_sample", "penalty_skipped", _sample_without_penalty, SAMPLING_PINS),
+       ("penalty_sample", "temperature_multiplied", _sample_temperature_multiplied, SAMPLING_PINS)]
 )
 
 

@@ -16,6 +16,8 @@
  *                        compacted cache (optionally appending the
  *                        new token first)                            (Sec. 1, 3.2)
  *   reco_logit_penalty   banded reflection-token logit penalty       (Eq. 3, 4)
+ *   reco_penalty_sample  the same penalty, then the next token drawn
+ *                        from softmax(z~ / T), one pass per row      (Eq. 4, Sec. 3.3)
  *   reco_answer_ppl      answer perplexity and stop flag             (Eq. 5, 6)
  *
  * Conventions shared by every call
@@ -59,7 +61,7 @@
 extern "C" {
 #endif
 
-#define RECO_ABI_VERSION 1
+#define RECO_ABI_VERSION 2
 
 typedef enum reco_status {
   RECO_OK = 0,
@@ -78,7 +80,8 @@ enum {
   RECO_DEV_BAD_RETENTION = 2,    /* retention r not in (0, 1] (or NaN) */
   RECO_DEV_BAD_SCORE = 3,        /* NaN or negative importance score */
   RECO_DEV_BAD_TOKEN_ID = 4,     /* reflection id or answer token outside [0, vocab) */
-  RECO_DEV_BAD_LENGTH = 5        /* stored len outside [0, capacity] */
+  RECO_DEV_BAD_LENGTH = 5,       /* stored len outside [0, capacity] */
+  RECO_DEV_BAD_LOGIT = 6         /* a logit row with no non-NaN value to sample */
 };
 
 /* reco_score flags */
@@ -175,6 +178,35 @@ reco_status_t reco_logit_penalty(float *logits, int32_t rows, int32_t vocab, int
                                  const int32_t *refl_ids, int32_t n_refl, const float *reward,
                                  float tau_lo, float tau_hi, float beta_lo, float beta_mid,
                                  float beta_hi, int32_t *dev_err, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Eq. 3 and Eq. 4, then sampling (Section 3.3: the next token is drawn from
+ * the softmax of the penalised logits), fused into one pass over each row.
+ * The penalty is exactly reco_logit_penalty's (written back in place,
+ * bit-exact).  Then
+ *   T == 0 : tokens[b] = argmax_u z~[b][u]   (greedy; lowest index on ties)
+ *   T  > 0 : tokens[b] = argmax_u (z~[b][u] / T + G[b][u])   (Gumbel-max,
+ *            an exact draw from softmax(z~[b] / T)), every step in fp32,
+ *            G = -log(-log U), U = ((x >> 9) + 1/2) * 2^-23, and x the
+ *            (u % 4)-th word of Philox4x32-10 (Salmon et al., SC 2011) on
+ *            counter (u / 4, b, offset low, offset high), key (seed low,
+ *            seed high).  (seed, offset, b, u) fixes the draw: advance
+ *            `offset` once per generated token for fresh noise.
+ *   logits   : [rows][ld] fp32, in place; ld >= vocab
+ *   refl_ids : [n_refl] int32, 0 <= n_refl <= 4096 (nullable when 0)
+ *   reward   : [rows] fp32
+ *   tokens   : [rows] int32 (output)
+ *   temperature : [host] finite, >= 0 (RECO_ERR_INVALID_ARG otherwise)
+ * NaN values never win; a row of NaNs gets token -1 and sets
+ * RECO_DEV_BAD_LOGIT.  An id outside [0, vocab) is skipped and sets
+ * RECO_DEV_BAD_TOKEN_ID.  rows <= 65535. */
+size_t reco_penalty_sample_workspace_size(int32_t rows, int32_t vocab);
+reco_status_t reco_penalty_sample(float *logits, int32_t rows, int32_t vocab, int64_t ld,
+                                  const int32_t *refl_ids, int32_t n_refl, const float *reward,
+                                  float tau_lo, float tau_hi, float beta_lo, float beta_mid,
+                                  float beta_hi, float temperature, uint64_t seed, uint64_t offset,
+                                  int32_t *tokens, void *ws, size_t ws_bytes, int32_t *dev_err,
+                                  hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Eq. 5 and Eq. 6 (Section 3.3, early stopping via answer confidence): for

@@ -27,11 +27,12 @@ RECO_F32 = 0
 RECO_BF16 = 1
 RECO_SCORE_CAUSAL = 1
 DEV_ERRORS = {0: "ok", 1: "append overflow", 2: "bad retention", 3: "bad score", 4: "bad token id",
-              5: "bad length"}
+              5: "bad length", 6: "bad logit row"}
 
 EXPORTED = [
     "reco_score_workspace_size", "reco_score", "reco_select_compact_workspace_size", "reco_select_compact",
     "reco_decode_attn_workspace_size", "reco_decode_attn", "reco_logit_penalty",
+    "reco_penalty_sample_workspace_size", "reco_penalty_sample",
     "reco_answer_ppl_workspace_size", "reco_answer_ppl", "reco_retention_from_reward", "reco_retention_eq1",
     "reco_kept_count", "reco_status_str", "reco_abi_version",
 ]
@@ -54,8 +55,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise RuntimeError(f"HIP library missing: {path} (build it with `python -m paper_2608_04771_amd.build`)")
     lib = ctypes.CDLL(path)
-    P, I32, I64, F32, F64, SZ, U32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
-                                      ctypes.c_double, ctypes.c_size_t, ctypes.c_uint32)
+    P, I32, I64, F32, F64, SZ, U32, U64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                           ctypes.c_double, ctypes.c_size_t, ctypes.c_uint32, ctypes.c_uint64)
     C = ctypes.POINTER(RecoKVCache)
     sig = {
         "reco_score_workspace_size": (SZ, [C, I32, I32, I32]),
@@ -65,6 +66,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "reco_decode_attn_workspace_size": (SZ, [C, I32, I32]),
         "reco_decode_attn": (I32, [C, I32, I32, P, I32, F32, P, P, P, P, P, SZ, P, P]),
         "reco_logit_penalty": (I32, [P, I32, I32, I64, P, I32, P, F32, F32, F32, F32, F32, P, P]),
+        "reco_penalty_sample_workspace_size": (SZ, [I32, I32]),
+        "reco_penalty_sample": (I32, [P, I32, I32, I64, P, I32, P, F32, F32, F32, F32, F32, F32, U64, U64, P, P, SZ,
+                                      P, P]),
         "reco_answer_ppl_workspace_size": (SZ, [I32, I32, I32]),
         "reco_answer_ppl": (I32, [P, P, I32, I32, I32, F32, P, P, P, SZ, P, P]),
         "reco_retention_from_reward": (F64, [F64, F64, F64]),
@@ -148,21 +152,24 @@ def decode_attn_workspace_size(cache: KVCache, n_q_heads: int, n_layers: Optiona
     return int(load_library().reco_decode_attn_workspace_size(cache.ref(), nl, n_q_heads))
 
 
+def penalty_sample_workspace_size(rows: int, vocab: int) -> int:
+    return int(load_library().reco_penalty_sample_workspace_size(rows, vocab))
+
+
 def answer_ppl_workspace_size(batch: int, n: int, vocab: int) -> int:
     return int(load_library().reco_answer_ppl_workspace_size(batch, n, vocab))
 
 
-def _ws(nbytes: int, device, ws: Optional[torch.Tensor], zero: bool = False) -> torch.Tensor:
+def _ws(nbytes: int, device, ws: Optional[torch.Tensor]) -> torch.Tensor:
     if ws is not None:
         return ws
-    alloc = torch.zeros if zero else torch.empty
-    return alloc(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
 
 
 def decode_workspace(cache: "KVCache", n_q_heads: int, n_layers: Optional[int] = None) -> torch.Tensor:
-    """A zero-filled decode workspace (its completion counters must start at 0;
-    every call leaves them at 0 again).  Do not share one between overlapping calls."""
-    return _ws(decode_attn_workspace_size(cache, n_q_heads, n_layers), cache.k.device, None, zero=True)
+    """A decode workspace (contents need not be initialised).  Do not share
+    one between overlapping calls."""
+    return _ws(decode_attn_workspace_size(cache, n_q_heads, n_layers), cache.k.device, None)
 
 
 def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[float] = None, causal: bool = True,
@@ -224,7 +231,7 @@ def reco_decode_attn(cache: KVCache, q: torch.Tensor, k_new: Optional[torch.Tens
     if lse is None and want_lse:
         lse = torch.empty((nl, B, hq), dtype=torch.float32, device=q.device)
     _need_cuda(q, k_new, v_new, out, lse, ws, dev_err)
-    ws = _ws(decode_attn_workspace_size(cache, hq, nl), q.device, ws, zero=True)
+    ws = _ws(decode_attn_workspace_size(cache, hq, nl), q.device, ws)
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     st = load_library().reco_decode_attn(cache.ref(), layer0, nl, _ptr(q), hq, scale, _ptr(k_new), _ptr(v_new),
                                          _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _ptr(dev_err),
@@ -251,6 +258,35 @@ def reco_logit_penalty(logits: torch.Tensor, refl_ids: torch.Tensor, reward: tor
                                            beta_hi, _ptr(dev_err), _stream(logits.device))
     _check(st, "reco_logit_penalty")
     return logits
+
+
+def reco_penalty_sample(logits: torch.Tensor, refl_ids: Optional[torch.Tensor], reward: torch.Tensor, tau_lo: float,
+                        tau_hi: float, beta_lo: float, beta_mid: float, beta_hi: float, temperature: float,
+                        seed: int, offset: int, tokens: Optional[torch.Tensor] = None,
+                        ws: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Eq. 3-4 in place on fp32 logits [rows][vocab], then the next token of
+    each row from softmax(z~ / T) (greedy when T = 0); returns tokens [rows] int32."""
+    if logits.dtype != torch.float32 or logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be fp32 [rows][vocab] with unit column stride")
+    if (refl_ids is not None and refl_ids.dtype != torch.int32) or reward.dtype != torch.float32:
+        raise ValueError("refl_ids int32, reward float32")
+    if not logits.is_cuda:
+        raise ValueError("logits must live on the GPU")
+    rows, vocab = logits.shape
+    if tokens is None:
+        tokens = torch.empty(rows, dtype=torch.int32, device=logits.device)
+    if tokens.dtype != torch.int32:
+        raise ValueError("tokens must be int32")
+    _need_cuda(refl_ids, reward, tokens, ws, dev_err)
+    ws = _ws(penalty_sample_workspace_size(rows, vocab), logits.device, ws)
+    n_refl = 0 if refl_ids is None else refl_ids.numel()
+    st = load_library().reco_penalty_sample(_ptr(logits), rows, vocab, logits.stride(0), _ptr(refl_ids), n_refl,
+                                            _ptr(reward), tau_lo, tau_hi, beta_lo, beta_mid, beta_hi,
+                                            float(temperature), int(seed) & (2 ** 64 - 1),
+                                            int(offset) & (2 ** 64 - 1), _ptr(tokens), _ptr(ws), ws.numel(),
+                                            _ptr(dev_err), _stream(logits.device))
+    _check(st, "reco_penalty_sample")
+    return tokens
 
 
 def reco_answer_ppl(logits: torch.Tensor, tokens: torch.Tensor, tau_p: float, ppl: Optional[torch.Tensor] = None,

@@ -230,6 +230,27 @@ reco_status_t reco_logit_penalty(float *logits, int32_t rows, int32_t vocab, int
                                                beta_lo, beta_mid, beta_hi, dev_err, stream));
 }
 
+// ---------------------------------------------------------------- penalty + sampling
+size_t reco_penalty_sample_workspace_size(int32_t rows, int32_t vocab) {
+  if (rows < 1 || vocab < 1) return 0;
+  return reco::penalty_sample_workspace_bytes(rows, vocab);
+}
+
+reco_status_t reco_penalty_sample(float *logits, int32_t rows, int32_t vocab, int64_t ld, const int32_t *refl_ids,
+                                  int32_t n_refl, const float *reward, float tau_lo, float tau_hi, float beta_lo,
+                                  float beta_mid, float beta_hi, float temperature, uint64_t seed, uint64_t offset,
+                                  int32_t *tokens, void *ws, size_t ws_bytes, int32_t *dev_err, hipStream_t stream) {
+  if (!logits || !reward || !tokens || rows < 1 || rows > 65535 || vocab < 1 || ld < vocab)
+    return RECO_ERR_INVALID_ARG;
+  if (n_refl < 0 || n_refl > 4096 || (n_refl > 0 && !refl_ids)) return RECO_ERR_INVALID_ARG;
+  if (!(temperature >= 0.f) || !isfinite(temperature)) return RECO_ERR_INVALID_ARG;
+  const size_t need = reco::penalty_sample_workspace_bytes(rows, vocab);
+  if (!ws || ws_bytes < need) return RECO_ERR_WORKSPACE;
+  return hip_status(reco::launch_penalty_sample(logits, rows, vocab, ld, refl_ids, n_refl, reward, tau_lo, tau_hi,
+                                                beta_lo, beta_mid, beta_hi, temperature, seed, offset, tokens, ws,
+                                                dev_err, stream));
+}
+
 // ---------------------------------------------------------------- answer PPL
 size_t reco_answer_ppl_workspace_size(int32_t batch, int32_t n, int32_t vocab) {
   if (batch < 1 || n < 1 || vocab < 1) return 0;

@@ -1,5 +1,6 @@
 // Generation-side kernels of Section 3.3 (gfx950):
 //   reflection-token penalty, Eq. 3 (reward band) and Eq. 4 (subtract beta);
+//   the same penalty fused with drawing the next token from softmax(z~ / T);
 //   answer perplexity, Eq. 5, and the stop rule, Eq. 6.
 #include "reco_device.hpp"
 #include "reco_kernels.hpp"
@@ -35,6 +36,162 @@ __global__ __launch_bounds__(kPenThreads) void logit_penalty_kernel(float *logit
     bool first = true;  // R is a set: only the first occurrence of an id subtracts
     for (int j = 0; j < i; ++j) first = first && (s_ids[j] != u);
     if (first) z[u] = z[u] - beta;
+  }
+}
+
+// ---- fused penalty + sampling ------------------------------------------------
+//
+// One pass over each logit row: Eq. 3 picks beta from the row's reward, Eq. 4
+// subtracts it from the reflection ids (written back in place, as the plain
+// penalty does), and the next token is the argmax of z~ (T = 0) or, for
+// T > 0, the Gumbel-max draw argmax(z~ / T + G), which is an exact sample of
+// softmax(z~ / T).  G = -log(-log U) with U from Philox4x32-10.  Workgroups
+// take 4096-element chunks of a row and leave (best value, index) partials; a
+// one-wave-per-row kernel merges them.  Ties and equal partials go to the
+// lowest index; NaN values never win.
+
+constexpr int kSmpThreads = 256;
+constexpr int kSmpChunk = 4096;                    // logits per workgroup
+constexpr int kSmpPerThread = kSmpChunk / kSmpThreads;   // 16 = four Philox blocks of 4
+constexpr int kSmpBitWords = kSmpChunk / 32;
+
+// Philox4x32 with 10 rounds (Salmon, Moraes, Dror and Shaw, SC 2011): each
+// round multiplies counter words 0 and 2 by the two round constants, crosses
+// the 64-bit products' halves with words 1 and 3 and the key, and the key
+// advances by the Weyl increments between rounds.
+__device__ __forceinline__ void philox4x32_10(uint32_t (&c)[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint32_t a = c[0], b = c[2];
+    const uint32_t lo0 = 0xD2511F53u * a, hi0 = __umulhi(0xD2511F53u, a);
+    const uint32_t lo1 = 0xCD9E8D57u * b, hi1 = __umulhi(0xCD9E8D57u, b);
+    c[0] = hi1 ^ c[1] ^ k0;
+    c[1] = lo1;
+    c[2] = hi0 ^ c[3] ^ k1;
+    c[3] = lo0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+}
+
+// Midpoint of one of 2^23 equal cells of (0, 1): exact in fp32, never 0 or 1.
+__device__ __forceinline__ float unit_open(uint32_t x) {
+  return static_cast<float>(x >> 9) * 0x1.0p-23f + 0x1.0p-24f;
+}
+
+__device__ __forceinline__ void arg_better(float &v, int &i, float v2, int i2) {
+  if (v2 > v || (v2 == v && i2 < i)) {
+    v = v2;
+    i = i2;
+  }
+}
+
+__device__ __forceinline__ void wave_argmax(float &v, int &i) {
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) {
+    const float v2 = __shfl_xor(v, m, kWave);
+    const int i2 = __shfl_xor(i, m, kWave);
+    arg_better(v, i, v2, i2);
+  }
+}
+
+struct SamplePart {
+  float v;
+  int32_t i;
+};
+
+__global__ __launch_bounds__(kSmpThreads) void penalty_sample_partial_kernel(
+    float *logits, int vocab, int64_t ld, const int32_t *ids, int n_ids, const float *reward, float tau_lo,
+    float tau_hi, float b_lo, float b_mid, float b_hi, float temperature, uint32_t seed_lo, uint32_t seed_hi,
+    uint32_t off_lo, uint32_t off_hi, int chunks, SamplePart *part, int32_t *dev_err) {
+  __shared__ uint32_t s_bits[kSmpBitWords];
+  __shared__ SamplePart s_red[kSmpThreads / kWave];
+  const int chunk = blockIdx.x;
+  const int row = blockIdx.y;
+  const int c0 = chunk * kSmpChunk;
+  for (int i = threadIdx.x; i < kSmpBitWords; i += kSmpThreads) s_bits[i] = 0u;
+  __syncthreads();
+  // Mark the reflection ids that fall in this chunk; a set, so duplicates merge.
+  for (int i = threadIdx.x; i < n_ids; i += kSmpThreads) {
+    const int u = ids[i];
+    if (u < 0 || u >= vocab) {
+      if (chunk == 0) report(dev_err, 4 /*RECO_DEV_BAD_TOKEN_ID*/);
+      continue;
+    }
+    const int r = u - c0;
+    if (r >= 0 && r < kSmpChunk) atomicOr(&s_bits[r >> 5], 1u << (r & 31));
+  }
+  __syncthreads();
+  const float v = reward[row];
+  const float beta = (v <= tau_lo) ? b_lo : ((v >= tau_hi) ? b_hi : b_mid);   // Eq. 3 as written
+  float *z = logits + static_cast<int64_t>(row) * ld;
+  const bool greedy = temperature == 0.f;
+
+  float best = -INFINITY;
+  int best_i = 0x7fffffff;
+#pragma unroll
+  for (int p = 0; p < kSmpPerThread / 4; ++p) {
+    const int r0 = (p * kSmpThreads + threadIdx.x) * 4;   // chunk-relative, multiple of 4
+    const int j0 = c0 + r0;
+    if (j0 >= vocab) break;
+    float x[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = (j0 + e < vocab) ? z[j0 + e] : -INFINITY;
+    const uint32_t bits = (s_bits[r0 >> 5] >> (r0 & 31)) & 0xFu;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if ((bits >> e) & 1u) {                                // Eq. 4, one fp32 subtraction
+        x[e] = x[e] - beta;
+        z[j0 + e] = x[e];
+      }
+    if (greedy) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (j0 + e < vocab) arg_better(best, best_i, x[e], j0 + e);
+    } else {
+      uint32_t c[4] = {static_cast<uint32_t>(j0 >> 2), static_cast<uint32_t>(row), off_lo, off_hi};
+      philox4x32_10(c, seed_lo, seed_hi);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float g = -logf(-logf(unit_open(c[e])));
+        const float y = x[e] / temperature + g;
+        if (j0 + e < vocab) arg_better(best, best_i, y, j0 + e);
+      }
+    }
+  }
+  wave_argmax(best, best_i);
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  if (lane == 0) s_red[wave] = SamplePart{best, best_i};
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    SamplePart r = s_red[0];
+#pragma unroll
+    for (int w = 1; w < kSmpThreads / kWave; ++w) arg_better(r.v, r.i, s_red[w].v, s_red[w].i);
+    part[static_cast<size_t>(row) * chunks + chunk] = r;
+  }
+}
+
+// One wave per row: merge the chunk partials into the row's token.
+__global__ __launch_bounds__(kSmpThreads) void penalty_sample_final_kernel(const SamplePart *part, int rows,
+                                                                           int chunks, int32_t *tokens,
+                                                                           int32_t *dev_err) {
+  const int row = blockIdx.x * (kSmpThreads / kWave) + threadIdx.x / kWave;
+  const int lane = threadIdx.x & (kWave - 1);
+  if (row >= rows) return;
+  float best = -INFINITY;
+  int best_i = 0x7fffffff;
+  for (int c = lane; c < chunks; c += kWave) {
+    const SamplePart q = part[static_cast<size_t>(row) * chunks + c];
+    arg_better(best, best_i, q.v, q.i);
+  }
+  wave_argmax(best, best_i);
+  if (lane == 0) {
+    if (best_i == 0x7fffffff) {             // every value of the row was NaN
+      report(dev_err, 6 /*RECO_DEV_BAD_LOGIT*/);
+      best_i = -1;
+    }
+    tokens[row] = best_i;
   }
 }
 
@@ -125,6 +282,29 @@ hipError_t launch_logit_penalty(float *logits, int rows, int vocab, int64_t ld, 
                                 float b_hi, int32_t *dev_err, hipStream_t s) {
   hipLaunchKernelGGL(logit_penalty_kernel, dim3(rows), dim3(kPenThreads), 0, s, logits, vocab, ld, ids, n_ids,
                      reward, tau_lo, tau_hi, b_lo, b_mid, b_hi, dev_err);
+  return hipGetLastError();
+}
+
+size_t penalty_sample_workspace_bytes(int rows, int vocab) {
+  const size_t chunks = static_cast<size_t>((vocab + kSmpChunk - 1) / kSmpChunk);
+  return static_cast<size_t>(rows) * chunks * sizeof(SamplePart);
+}
+
+hipError_t launch_penalty_sample(float *logits, int rows, int vocab, int64_t ld, const int32_t *ids, int n_ids,
+                                 const float *reward, float tau_lo, float tau_hi, float b_lo, float b_mid,
+                                 float b_hi, float temperature, uint64_t seed, uint64_t offset, int32_t *tokens,
+                                 void *ws, int32_t *dev_err, hipStream_t s) {
+  const int chunks = (vocab + kSmpChunk - 1) / kSmpChunk;
+  SamplePart *part = reinterpret_cast<SamplePart *>(ws);
+  hipLaunchKernelGGL(penalty_sample_partial_kernel, dim3(chunks, rows), dim3(kSmpThreads), 0, s, logits, vocab, ld,
+                     ids, n_ids, reward, tau_lo, tau_hi, b_lo, b_mid, b_hi, temperature,
+                     static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32), static_cast<uint32_t>(offset),
+                     static_cast<uint32_t>(offset >> 32), chunks, part, dev_err);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int per_wg = kSmpThreads / kWave;
+  hipLaunchKernelGGL(penalty_sample_final_kernel, dim3((rows + per_wg - 1) / per_wg), dim3(kSmpThreads), 0, s, part,
+                     rows, chunks, tokens, dev_err);
   return hipGetLastError();
 }
 

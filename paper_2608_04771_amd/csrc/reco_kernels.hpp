@@ -67,6 +67,13 @@ hipError_t launch_logit_penalty(float *logits, int rows, int vocab, int64_t ld, 
                                 float b_lo, float b_mid, float b_hi, int32_t *dev_err,
                                 hipStream_t s);
 
+// ---- fused penalty + sampling -----------------------------------------------
+size_t penalty_sample_workspace_bytes(int rows, int vocab);
+hipError_t launch_penalty_sample(float *logits, int rows, int vocab, int64_t ld, const int32_t *ids, int n_ids,
+                                 const float *reward, float tau_lo, float tau_hi, float b_lo, float b_mid,
+                                 float b_hi, float temperature, uint64_t seed, uint64_t offset, int32_t *tokens,
+                                 void *ws, int32_t *dev_err, hipStream_t s);
+
 // ---- answer perplexity -----------------------------------------------------------
 size_t ppl_workspace_bytes(int batch, int n, int vocab);
 hipError_t launch_answer_ppl(const float *logits, const int32_t *tokens, int batch, int n, int vocab,

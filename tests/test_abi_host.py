@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     lib = B.load_library()
-    assert B.reco_abi_version() == 1
+    assert B.reco_abi_version() == 2
     assert lib.reco_status_str(0) == b"ok"
     assert b"workspace" in lib.reco_status_str(3)
     assert lib.reco_status_str(99) == b"unknown status"
@@ -151,6 +151,30 @@ def test_penalty_and_ppl_reject_bad_arguments():
     assert ppl(out=0) == B.RECO_ERR_INVALID_ARG
     assert ppl(ws=0) == B.RECO_ERR_WORKSPACE
     assert ppl(wsb=4) == B.RECO_ERR_WORKSPACE
+
+
+def test_penalty_sample_rejects_bad_arguments():
+    lib = B.load_library()
+    need = lib.reco_penalty_sample_workspace_size(3, 128256)
+    assert need >= 3 * 32 * 8
+    assert lib.reco_penalty_sample_workspace_size(0, 10) == 0
+
+    def smp(logits=0x10, rows=3, vocab=128256, ld=128256, ids=0x20, n=4, rew=0x30, T=1.0, tok=0x40, ws=0x50,
+            wsb=need):
+        return lib.reco_penalty_sample(P(logits), rows, vocab, ld, P(ids), n, P(rew), 0.4, 0.8, 0.0, 1.0, 3.0, T,
+                                       2 ** 63 + 5, 2 ** 40, P(tok), P(ws), wsb, None, None)
+    assert smp(logits=0) == B.RECO_ERR_INVALID_ARG
+    assert smp(tok=0) == B.RECO_ERR_INVALID_ARG
+    assert smp(rew=0) == B.RECO_ERR_INVALID_ARG
+    assert smp(rows=0) == B.RECO_ERR_INVALID_ARG
+    assert smp(rows=65536) == B.RECO_ERR_INVALID_ARG
+    assert smp(ld=128255) == B.RECO_ERR_INVALID_ARG
+    assert smp(n=4097) == B.RECO_ERR_INVALID_ARG
+    assert smp(n=2, ids=0) == B.RECO_ERR_INVALID_ARG
+    for bad_t in (-0.5, float("nan"), float("inf"), -0.0 - 1e-30):
+        assert smp(T=bad_t) == B.RECO_ERR_INVALID_ARG, bad_t
+    assert smp(ws=0) == B.RECO_ERR_WORKSPACE
+    assert smp(wsb=need - 1) == B.RECO_ERR_WORKSPACE
 
 
 def test_workspace_sizes_are_positive_and_monotone():

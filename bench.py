@@ -5,7 +5,8 @@ One step = one pass of the whole path over one batch of synthetic input:
   window scoring (Eq. 2) -> reward-budgeted selection + in-place compaction
   -> `decode_steps` decode-attention calls over all layers (each appending the
   new token) with the banded reflection-logit penalty (Eq. 3-4) on that
-  step's logit row -> one answer-perplexity probe (Eq. 5-6).
+  step's logit row and the next token drawn from softmax(z~) (one fused
+  pass per row) -> one answer-perplexity probe (Eq. 5-6).
 Every step starts from its own pristine copy of the cache, staged in HBM
 before the timed region.  Prints one JSON line (rank 0, N = 1).
 
@@ -34,6 +35,8 @@ PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E vendor peak
 METRIC = "compress+decode-attn KV tokens/s and achieved HBM GB/s (% of peak), 1 GPU"
 TAU_LO, TAU_HI, TAU_P = 0.4, 0.8, 1.1          # Section 4.1
 BETAS = (0.0, 1.0, 3.0)                        # penalty per reward band
+TEMPERATURE = 1.0                              # sample from softmax(z~) itself
+SAMPLE_SEED = 0x5EED
 N_REFL = 64
 ANSWER_LEN = 32
 
@@ -44,10 +47,10 @@ ANSWER_LEN = 32
 # files change, the figure is reported as null until it is measured again.
 DECODE_TRAFFIC = {
     "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
-                "paper_2608_04771_amd/csrc/reco_kernels.hpp"),
-    "sha256": "a1b36a34efb9a4fe6fb3ae4e6d2b1f2e2eab9cccff3e0aebc2017ee2acc00685",
+                "paper_2608_04771_amd/csrc/decode_attn.hpp"),
+    "sha256": "2fb656c3a02644e4766d747b5b48ae6291724ac2158bbcd15e50f4173dfb8ef5",
     "workload": "7b-28L-28q4kv-d128-bf16-L16384",
-    "fetch_bytes": 555420213,
+    "fetch_bytes": 555323104,
     "write_bytes": 817152,
 }
 
@@ -103,6 +106,8 @@ class Workload:
         self.ws_sel = torch.empty(B.select_compact_workspace_size(c), dtype=torch.uint8, device=dev)
         self.ws_dec = B.decode_workspace(c, wl.n_q_heads)
         self.ws_ppl = torch.empty(B.answer_ppl_workspace_size(Bsz, ANSWER_LEN, V), dtype=torch.uint8, device=dev)
+        self.ws_smp = torch.empty(B.penalty_sample_workspace_size(Bsz, V), dtype=torch.uint8, device=dev)
+        self.tokens = torch.empty((wl.decode_steps, Bsz), dtype=torch.int32, device=dev)
         self.out = torch.empty_like(self.q[0])
         self.lse = torch.empty(self.q.shape[1:4], dtype=torch.float32, device=dev)
         self.ppl = torch.empty(Bsz, dtype=torch.float32, device=dev)
@@ -111,10 +116,10 @@ class Workload:
         self.side = torch.cuda.Stream(device=dev)       # default priority
 
     def step(self, i, ev=None):
-        """One pass of the hot path on cache copy i.  The reflection penalties
-        of the decode steps run on a side stream (they are independent of the
-        attention) and join the main stream before the answer probe.  `ev`
-        optionally collects HIP events on the main stream around the phases."""
+        """One pass of the hot path on cache copy i.  The penalise-and-sample
+        passes of the decode steps run on a side stream (they are independent
+        of the attention) and join the main stream before the answer probe.
+        `ev` optionally collects HIP events on the main stream around the phases."""
         wl = self.wl
         cache = B.KVCache(*self.copies[i])
         main = torch.cuda.current_stream()
@@ -130,8 +135,9 @@ class Workload:
         self.side.wait_stream(main)
         with torch.cuda.stream(self.side):
             for s in range(wl.decode_steps):
-                B.reco_logit_penalty(self.logits[s], self.refl, self.step_reward, TAU_LO, TAU_HI, *BETAS,
-                                     dev_err=self.dev_err)
+                B.reco_penalty_sample(self.logits[s], self.refl, self.step_reward, TAU_LO, TAU_HI, *BETAS,
+                                      TEMPERATURE, SAMPLE_SEED, s, tokens=self.tokens[s], ws=self.ws_smp,
+                                      dev_err=self.dev_err)
         for s in range(wl.decode_steps):
             B.reco_decode_attn(cache, self.q[s], self.k_new[s], self.v_new[s], out=self.out, lse=self.lse,
                                ws=self.ws_dec, dev_err=self.dev_err)
@@ -166,7 +172,7 @@ def algorithmic_bytes(w: Workload, m: np.ndarray, moved_rows: int):
     for s in range(wl.decode_steps):
         rows = int((m + s + 1).sum())                 # keys attended (cached + new) over all units
         dec.append(rows * 2 * D * e + 2 * NL * Bsz * Hq * D * e + NL * Bsz * Hq * 4 + 2 * m.size * D * e)
-    penalty = wl.decode_steps * Bsz * N_REFL * 4 * 2
+    penalty = wl.decode_steps * Bsz * (wl.vocab * 4 + N_REFL * 4 + 4)   # read the row, write R and the token
     ppl = Bsz * ANSWER_LEN * wl.vocab * 4
     return {"score": score, "select": select, "compact": compact, "decode": dec, "penalty": penalty, "ppl": ppl}
 

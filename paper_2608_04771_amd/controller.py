@@ -8,15 +8,17 @@ The paper's loop, per completed reasoning step i with process reward v_i:
   reward statistics (or by the fixed map r = clamp(1 - v/2, 0.3, 1));
 * attention-guided selection (Eq. 2) over the w most recent queries;
 * the reward band of the just-completed step sets the reflection-token
-  penalty applied to every logit row of the next step (Eq. 3-4);
+  penalty applied to every logit row of the next step (Eq. 3-4), and the
+  next token is drawn from the softmax of the penalised row;
 * two consecutive top-band rewards trigger the answer probe, whose
   perplexity decides the stop (Eq. 5-6).
 
 `RewardSchedule` holds the pure host bookkeeping (reward history, retention,
 compression trigger, probe trigger) and runs without a GPU.  `RecoDecoder`
 drives the kernels through the binding: it keeps the window queries in a ring
-buffer on the device, calls reco_decode_attn / reco_logit_penalty per token
-and reco_score / reco_select_compact at step boundaries.  All arithmetic of
+buffer on the device, calls reco_decode_attn and reco_logit_penalty (or the
+fused reco_penalty_sample) per token and reco_score / reco_select_compact at
+step boundaries.  All arithmetic of
 the method runs in the library; this module decides when, and moves data.
 """
 from __future__ import annotations
@@ -120,6 +122,8 @@ class RecoDecoder:
         self.dev_err = torch.zeros(1, dtype=torch.int32, device=dev)
         self.out = torch.empty((NL, Bsz, n_q_heads, D), dtype=cache.k.dtype, device=dev)
         self.lse = torch.empty((NL, Bsz, n_q_heads), dtype=torch.float32, device=dev)
+        self.tokens = torch.empty(Bsz, dtype=torch.int32, device=dev)
+        self.ws_smp = None
         # Positions 0..prompt_len-1 are in the cache; the ring's rows hold
         # prompt positions prompt_len - w .. prompt_len - 1 in order, i.e. the
         # row of position p is p % w once rotated into place.
@@ -144,6 +148,22 @@ class RecoDecoder:
         for s in self.sched:
             s.token_appended()
         return self.out, self.lse
+
+    def sample(self, logits: torch.Tensor, temperature: float = 1.0, seed: int = 0) -> torch.Tensor:
+        """The current reflection penalty on this token's logit rows ([B][vocab],
+        in place) and the next token of every sequence drawn from
+        softmax(z~ / T) (T = 0: greedy), in one fused pass.  The draw is keyed
+        by (seed, tokens seen so far), so call it once per decoded token.
+        Returns the tokens [B] int32 (a buffer reused by the next call)."""
+        if self.refl is None:
+            raise ValueError("sampling with the reflection penalty needs refl_ids")
+        rows, vocab = logits.shape
+        need = B.penalty_sample_workspace_size(rows, vocab)
+        if self.ws_smp is None or self.ws_smp.numel() < need:
+            self.ws_smp = torch.empty(need, dtype=torch.uint8, device=logits.device)
+        p = self.policy
+        return B.reco_penalty_sample(logits, self.refl, self.band_reward, p.tau_lo, p.tau_hi, *p.betas, temperature,
+                                     seed, self.count, tokens=self.tokens, ws=self.ws_smp, dev_err=self.dev_err)
 
     def window_queries(self) -> torch.Tensor:
         """The last w queries in order (row t = position L - w + t)."""

@@ -21,7 +21,7 @@
 // on this chip write back and invalidate the L2 that the streaming
 // workgroups depend on.
 #include "reco_device.hpp"
-#include "reco_kernels.hpp"
+#include "decode_attn.hpp"
 
 #include <math.h>
 

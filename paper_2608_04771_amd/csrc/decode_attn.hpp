@@ -1,0 +1,31 @@
+// Launch interface of the decode-attention kernels (decode_attn.hip), kept
+// apart from the other kernels' declarations.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace reco {
+
+// ---- decode attention ------------------------------------------------------
+struct DecodeParams {
+  void *k;                // cache K base (whole cache); the append commit writes it
+  void *v;                // cache V base
+  int32_t *len;           // [cache layers][batch][hkv]
+  const void *q;          // [n_layers][batch][hq][D]
+  const void *k_new;      // nullable [n_layers][batch][hkv][D]
+  const void *v_new;
+  void *out;              // [n_layers][batch][hq][D]
+  float *lse;             // nullable [n_layers][batch][hq]
+  float *part_o;          // [units][splits][16][D]
+  float *part_ml;         // [units][splits][32]  (16 maxima, 16 sums)
+  int32_t *dev_err;
+  int layer0, n_layers, batch, hkv, cap, group, hq, splits;
+  float scale_log2;       // logit scale * log2(e)
+};
+int decode_splits(int units, int capacity);
+size_t decode_workspace_bytes(int units, int capacity, int head_dim);
+hipError_t launch_decode(const DecodeParams &p, int dtype, int head_dim, hipStream_t s);
+
+}  // namespace reco

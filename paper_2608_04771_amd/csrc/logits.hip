@@ -46,13 +46,12 @@ __global__ __launch_bounds__(kPenThreads) void logit_penalty_kernel(float *logit
 // penalty does), and the next token is the argmax of z~ (T = 0) or, for
 // T > 0, the Gumbel-max draw argmax(z~ / T + G), which is an exact sample of
 // softmax(z~ / T).  G = -log(-log U) with U from Philox4x32-10.  Workgroups
-// take 4096-element chunks of a row and leave (best value, index) partials; a
-// one-wave-per-row kernel merges them.  Ties and equal partials go to the
+// take 1024-element chunks of a row (one Philox block of four per thread) and
+// leave (best value, index) partials; a one-wave-per-row kernel merges them.  Ties and equal partials go to the
 // lowest index; NaN values never win.
 
 constexpr int kSmpThreads = 256;
-constexpr int kSmpChunk = 4096;                    // logits per workgroup
-constexpr int kSmpPerThread = kSmpChunk / kSmpThreads;   // 16 = four Philox blocks of 4
+constexpr int kSmpChunk = kSmpThreads * 4;   // logits per workgroup: one Philox block of 4 per thread
 constexpr int kSmpBitWords = kSmpChunk / 32;
 
 // Philox4x32 with 10 rounds (Salmon, Moraes, Dror and Shaw, SC 2011): each
@@ -109,11 +108,20 @@ __global__ __launch_bounds__(kSmpThreads) void penalty_sample_partial_kernel(
   const int chunk = blockIdx.x;
   const int row = blockIdx.y;
   const int c0 = chunk * kSmpChunk;
-  for (int i = threadIdx.x; i < kSmpBitWords; i += kSmpThreads) s_bits[i] = 0u;
+  const int r0 = threadIdx.x * 4;                    // chunk-relative, multiple of 4
+  const int j0 = c0 + r0;
+  float *z = logits + static_cast<int64_t>(row) * ld;
+  // Issue every global load before the first barrier so their latencies overlap.
+  float x[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) x[e] = (j0 + e < vocab) ? z[j0 + e] : -INFINITY;
+  const float v = reward[row];
+  const int my_id = (static_cast<int>(threadIdx.x) < n_ids) ? ids[threadIdx.x] : -1;
+  if (threadIdx.x < kSmpBitWords) s_bits[threadIdx.x] = 0u;
   __syncthreads();
   // Mark the reflection ids that fall in this chunk; a set, so duplicates merge.
   for (int i = threadIdx.x; i < n_ids; i += kSmpThreads) {
-    const int u = ids[i];
+    const int u = (i == static_cast<int>(threadIdx.x)) ? my_id : ids[i];
     if (u < 0 || u >= vocab) {
       if (chunk == 0) report(dev_err, 4 /*RECO_DEV_BAD_TOKEN_ID*/);
       continue;
@@ -122,29 +130,19 @@ __global__ __launch_bounds__(kSmpThreads) void penalty_sample_partial_kernel(
     if (r >= 0 && r < kSmpChunk) atomicOr(&s_bits[r >> 5], 1u << (r & 31));
   }
   __syncthreads();
-  const float v = reward[row];
   const float beta = (v <= tau_lo) ? b_lo : ((v >= tau_hi) ? b_hi : b_mid);   // Eq. 3 as written
-  float *z = logits + static_cast<int64_t>(row) * ld;
-  const bool greedy = temperature == 0.f;
 
   float best = -INFINITY;
   int best_i = 0x7fffffff;
-#pragma unroll
-  for (int p = 0; p < kSmpPerThread / 4; ++p) {
-    const int r0 = (p * kSmpThreads + threadIdx.x) * 4;   // chunk-relative, multiple of 4
-    const int j0 = c0 + r0;
-    if (j0 >= vocab) break;
-    float x[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) x[e] = (j0 + e < vocab) ? z[j0 + e] : -INFINITY;
+  if (j0 < vocab) {
     const uint32_t bits = (s_bits[r0 >> 5] >> (r0 & 31)) & 0xFu;
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      if ((bits >> e) & 1u) {                                // Eq. 4, one fp32 subtraction
+      if ((bits >> e) & 1u) {                        // Eq. 4, one fp32 subtraction
         x[e] = x[e] - beta;
         z[j0 + e] = x[e];
       }
-    if (greedy) {
+    if (temperature == 0.f) {
 #pragma unroll
       for (int e = 0; e < 4; ++e)
         if (j0 + e < vocab) arg_better(best, best_i, x[e], j0 + e);

@@ -17,6 +17,7 @@ import torch
 import oracle
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd import inputs as I
+from paper_2608_04771_amd.controller import RecoDecoder, RecoPolicy
 
 pytestmark = pytest.mark.gpu
 
@@ -158,3 +159,38 @@ def test_offset_and_seed_give_fresh_draws():
     assert (a != b).sum() > rows // 2 and (a != c).sum() > rows // 2
     _, ref, vals = oracle.penalty_sample(full, [], reward, *TAU, *BETAS, 1.0, 1, 1)
     _assert_tokens(b, ref, vals, 1.0, "offset 1")
+
+
+def test_controller_samples_with_the_current_band():
+    """Decode + sample through the controller: each token's draw uses the band
+    of the last completed step and the noise keyed by (seed, position)."""
+    NL, Bsz, H, Hq, D, w, cap, prompt = 1, 3, 2, 4, 64, 8, 128, 40
+    vocab, seed, T = 3000, 99, 0.8
+    g = torch.Generator().manual_seed(5)
+    k = torch.zeros((NL, Bsz, H, cap, D))
+    v = torch.zeros_like(k)
+    k[:, :, :, :prompt] = torch.randn((NL, Bsz, H, prompt, D), generator=g)
+    v[:, :, :, :prompt] = torch.randn((NL, Bsz, H, prompt, D), generator=g)
+    ln = torch.full((NL, Bsz, H), prompt, dtype=torch.int32)
+    cache = B.KVCache(k.cuda(), v.cuda(), ln.cuda())
+    refl = I.make_reflection_ids(32, vocab, seed=6)
+    dec = RecoDecoder(cache, Hq, RecoPolicy(retention="clamp", window=w), torch.randn((NL, Bsz, Hq, w, D),
+                      generator=g).cuda(), torch.from_numpy(refl).cuda())
+    z_all = I.make_logits(30 * Bsz, vocab, seed=7).numpy().reshape(30, Bsz, vocab)
+    band = np.zeros(Bsz, dtype=np.float32)
+    rewards = {9: [0.1, 0.5, 0.9], 19: [0.95, 0.3, 0.85]}
+    for t in range(30):
+        q = torch.randn((NL, Bsz, Hq, D), generator=g).cuda()
+        kn = torch.randn((NL, Bsz, H, D), generator=g).cuda()
+        vn = torch.randn((NL, Bsz, H, D), generator=g).cuda()
+        dec.decode(q, kn, vn)
+        z = torch.from_numpy(z_all[t].copy()).cuda()
+        pos = dec.count
+        tok = dec.sample(z, temperature=T, seed=seed).cpu().numpy().astype(np.int64)
+        zp, ref, vals = oracle.penalty_sample(z_all[t], refl, band, *TAU, *BETAS, T, seed, pos)
+        assert z.cpu().numpy().tobytes() == zp.tobytes(), t
+        _assert_tokens(tok, ref, vals, T, f"token {t}")
+        if t in rewards:
+            dec.end_step(rewards[t])
+            band = np.array(rewards[t], dtype=np.float32)
+    assert dec.dev_err.item() == 0

@@ -40,6 +40,7 @@ __all__ = [
     "retention_from_reward", "retention_eq1", "kept_count", "score_unit", "select_unit",
     "compact_unit", "decode_unit", "penalty_band", "logit_penalty", "answer_ppl",
     "philox4x32_10", "uniform_from_bits", "gumbel_noise", "penalty_sample",
+    "layer_retention", "pool_scores",
 ]
 
 
@@ -78,6 +79,21 @@ def kept_count(L: int, w: int, r: float) -> int:
         raise ValueError("retention must lie in (0, 1]")
     w_eff = min(int(w), int(L))
     return min(int(L), max(w_eff, math.ceil(float(r) * float(L))))
+
+
+def layer_retention(r: float, layer: int, n_layers: int, spread: float) -> float:
+    """Per-layer budgets, a policy variant on the same kernels (the pyramid
+    idea the paper cites among classical eviction methods, Section 1): the
+    retention falls linearly with depth from r(1 + spread) at layer 0 to
+    r(1 - spread) at the last layer, so its mean over layers is r, and is
+    capped at 1 (a cap lowers the mean).  spread = 0 is the paper's single
+    retention level; 0 <= spread < 1."""
+    if not (0.0 <= spread < 1.0):
+        raise ValueError("spread must lie in [0, 1)")
+    if n_layers == 1:
+        return min(1.0, float(r))
+    t = float(layer) / float(n_layers - 1)
+    return min(1.0, float(r) * (1.0 + float(spread) * (1.0 - 2.0 * t)))
 
 
 # ---------------------------------------------------------------------------
@@ -132,6 +148,25 @@ def select_unit(s: np.ndarray, L: int, w: int, r: float) -> np.ndarray:
     order = np.lexsort((np.arange(P), -prefix))                  # score desc, then position asc
     kept = np.sort(order[:k])
     return np.concatenate([kept, np.arange(P, L)]).astype(np.int64)
+
+
+def pool_scores(s: np.ndarray, L: int, w: int, kernel: int, mode: str) -> np.ndarray:
+    """Score pooling before the top-k, a policy variant on the same kernels
+    (the clustering idea of SnapKV, cited in Section 1): each prefix position
+    j < P = L - min(w, L) takes the max ("max") or the mean ("mean") of s
+    over the prefix positions i with |i - j| <= kernel // 2; window positions
+    keep their own score (the window is always kept).  kernel is odd."""
+    L = int(L)
+    P = L - min(int(w), L)
+    h = int(kernel) // 2
+    s = np.asarray(s, dtype=np.float64)
+    out = s[:L].copy()
+    if P == 0:
+        return out
+    padded = np.concatenate([np.full(h, np.nan), s[:P], np.full(h, np.nan)])
+    win = np.lib.stride_tricks.sliding_window_view(padded, 2 * h + 1)    # [P][kernel], NaN outside the prefix
+    out[:P] = np.nanmax(win, axis=1) if mode == "max" else np.nanmean(win, axis=1)
+    return out
 
 
 def compact_unit(K: np.ndarray, V: np.ndarray, idx: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
@@ -245,7 +280,8 @@ def score_cache(K: np.ndarray, lens: np.ndarray, Qwin: np.ndarray, scale: float,
 
 def compress_cache(K: np.ndarray, V: np.ndarray, lens: np.ndarray, Qwin: np.ndarray,
                    retention: Sequence[float], w: int, scale: float, causal: bool = True):
-    """Score, select and compact every unit (retention r is per sequence).
+    """Score, select and compact every unit (retention r is per sequence,
+    ``retention[b]``, or per layer and sequence, ``retention[l][b]``).
 
     Returns (s, idx, K2, V2, lens2): scores, the kept index list of every unit
     (dict keyed by (layer, seq, head)), the compacted caches (rows >= m keep
@@ -258,7 +294,8 @@ def compress_cache(K: np.ndarray, V: np.ndarray, lens: np.ndarray, Qwin: np.ndar
         for b in range(B):
             for h in range(H):
                 L = int(lens[l, b, h])
-                sel = select_unit(s[l, b, h], L, w, float(retention[b]))
+                r = retention[b] if np.ndim(retention) == 1 else retention[l][b]
+                sel = select_unit(s[l, b, h], L, w, float(r))
                 idx[(l, b, h)] = sel
                 kk, vv = compact_unit(K[l, b, h], V[l, b, h], sel)
                 K2[l, b, h, :len(sel)] = kk

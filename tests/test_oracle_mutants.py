@@ -12,11 +12,13 @@ import pytest
 import oracle
 import oracle.reco_oracle as ro
 import test_oracle_pins as pins
+import test_oracle_policy as ppins
 import test_oracle_sampling as spins
 
 _ORIG_PPL = ro.answer_ppl
 _ORIG_GUMBEL = ro.gumbel_noise
 _ORIG_PENALTY = ro.logit_penalty
+_ORIG_POOL = ro.pool_scores
 
 
 # ----------------------------------------------------------------- mutants
@@ -248,6 +250,61 @@ def _sample_temperature_multiplied(z, refl_ids, reward, tau_lo, tau_hi, b_lo, b_
     return zp, np.argmax(vals, axis=1), vals
 
 
+def _layer_ret_ascending(r, layer, n_layers, spread):
+    # planted: the slope runs the wrong way (more cache at the top layers)
+    t = 0.0 if n_layers == 1 else layer / (n_layers - 1)
+    return min(1.0, r * (1.0 - spread * (1.0 - 2.0 * t)))
+
+
+def _layer_ret_uncapped(r, layer, n_layers, spread):
+    t = 0.0 if n_layers == 1 else layer / (n_layers - 1)
+    return r * (1.0 + spread * (1.0 - 2.0 * t))                       # planted: no cap at 1
+
+
+def _layer_ret_half_slope(r, layer, n_layers, spread):
+    t = 0.0 if n_layers == 1 else layer / (n_layers - 1)
+    return min(1.0, r * (1.0 + spread * (1.0 - t)))                   # planted: mean is not r
+
+
+def _pool_including_window(s, L, w, kernel, mode):
+    # planted: the window positions take part in the pooling
+    return _ORIG_POOL(s, L, 0, kernel, mode)[:L] if L else np.zeros(0)
+
+
+def _pool_wide(s, L, w, kernel, mode):
+    return _ORIG_POOL(s, L, w, kernel + 2, mode)                     # planted: half width off by one
+
+
+def _pool_mean_over_kernel(s, L, w, kernel, mode):
+    # planted: the mean divides by the kernel size even where the window is cut at the edges
+    out = _ORIG_POOL(s, L, w, kernel, mode)
+    if mode != "mean":
+        return out
+    P = L - min(w, L)
+    h = kernel // 2
+    for j in range(P):
+        cnt = min(P, j + h + 1) - max(0, j - h)
+        out[j] = out[j] * cnt / kernel
+    return out
+
+
+def _pool_shifted(s, L, w, kernel, mode):
+    # planted: the pooling window is not centred (covers j .. j + kernel - 1)
+    s = np.asarray(s, dtype=np.float64)
+    out = s[:L].copy()
+    P = L - min(w, L)
+    for j in range(P):
+        seg = s[j:min(P, j + kernel)]
+        out[j] = seg.max() if mode == "max" else seg.mean()
+    return out
+
+
+LAYER_PINS = [ppins.test_layer_retention_is_a_descending_line_with_mean_r, ppins.test_layer_retention_cap_and_edges,
+              ppins.test_compress_cache_takes_per_layer_retention]
+POOL_PINS = [ppins.test_pool_kernel_one_is_identity_and_constant_stays_constant,
+             ppins.test_pool_max_spreads_a_spike_over_the_kernel_width, ppins.test_pool_mean_of_a_ramp_is_the_ramp_inside,
+             ppins.test_pool_leaves_the_window_alone_and_ignores_it]
+
 SAMPLING_PINS = [spins.test_gumbel_noise_moments, spins.test_greedy_is_argmax_of_penalised_logits,
                  spins.test_sampling_distribution_is_softmax_of_penalised_logits]
 
@@ -269,7 +326,14 @@ CASES = (
         [spins.test_uniform_grid_is_open_and_symmetric]),
        ("uniform_from_bits", "grid_of_24_bits", _uniform_24_bits, [spins.test_uniform_grid_is_open_and_symmetric]),
        ("penalty_sample", "penalty_skipped", _sample_without_penalty, SAMPLING_PINS),
-       ("penalty_sample", "temperature_multiplied", _sample_temperature_multiplied, SAMPLING_PINS)]
+       ("penalty_sample", "temperature_multiplied", _sample_temperature_multiplied, SAMPLING_PINS),
+       ("layer_retention", "ascending", _layer_ret_ascending, LAYER_PINS),
+       ("layer_retention", "uncapped", _layer_ret_uncapped, LAYER_PINS),
+       ("layer_retention", "half_slope", _layer_ret_half_slope, LAYER_PINS),
+       ("pool_scores", "includes_window", _pool_including_window, POOL_PINS),
+       ("pool_scores", "too_wide", _pool_wide, POOL_PINS),
+       ("pool_scores", "mean_over_kernel_size", _pool_mean_over_kernel, POOL_PINS),
+       ("pool_scores", "not_centred", _pool_shifted, POOL_PINS)]
 )
 
 

@@ -4,9 +4,9 @@
 One step = one pass of the whole path over one batch of synthetic input:
   window scoring (Eq. 2) -> reward-budgeted selection + in-place compaction
   -> `decode_steps` decode-attention calls over all layers (each appending the
-  new token) with the banded reflection-logit penalty (Eq. 3-4) on that
-  step's logit row and the next token drawn from softmax(z~) (one fused
-  pass per row) -> one answer-perplexity probe (Eq. 5-6).
+  new token), the banded reflection-logit penalty (Eq. 3-4) on every
+  generated token's logit row with the next token drawn from softmax(z~)
+  (one fused pass over the rows) -> one answer-perplexity probe (Eq. 5-6).
 Every step starts from its own pristine copy of the cache, staged in HBM
 before the timed region.  Prints one JSON line (rank 0, N = 1).
 
@@ -94,6 +94,8 @@ class Workload:
         self.logits = I.make_logits(wl.decode_steps * Bsz, V, seed=wl.seed + 17).to(dev).view(wl.decode_steps, Bsz, V)
         self.refl = torch.from_numpy(I.make_reflection_ids(N_REFL, V, seed=wl.seed + 19)).to(dev)
         self.step_reward = torch.from_numpy(ci.reward.astype(np.float32)).to(dev)
+        # every generated token of the step is penalised with the band of the step's reward
+        self.row_reward = self.step_reward.repeat(wl.decode_steps).contiguous()
         self.ans_logits = I.make_logits(Bsz * ANSWER_LEN, V, seed=wl.seed + 23,
                                         shape=(Bsz, ANSWER_LEN, V)).to(dev)
         self.ans_tok = torch.from_numpy(I.make_answer_tokens(Bsz, ANSWER_LEN, V, seed=wl.seed + 29)).to(dev)
@@ -106,8 +108,9 @@ class Workload:
         self.ws_sel = torch.empty(B.select_compact_workspace_size(c), dtype=torch.uint8, device=dev)
         self.ws_dec = B.decode_workspace(c, wl.n_q_heads)
         self.ws_ppl = torch.empty(B.answer_ppl_workspace_size(Bsz, ANSWER_LEN, V), dtype=torch.uint8, device=dev)
-        self.ws_smp = torch.empty(B.penalty_sample_workspace_size(Bsz, V), dtype=torch.uint8, device=dev)
-        self.tokens = torch.empty((wl.decode_steps, Bsz), dtype=torch.int32, device=dev)
+        self.ws_smp = torch.empty(B.penalty_sample_workspace_size(wl.decode_steps * Bsz, V), dtype=torch.uint8,
+                                  device=dev)
+        self.tokens = torch.empty(wl.decode_steps * Bsz, dtype=torch.int32, device=dev)
         self.out = torch.empty_like(self.q[0])
         self.lse = torch.empty(self.q.shape[1:4], dtype=torch.float32, device=dev)
         self.ppl = torch.empty(Bsz, dtype=torch.float32, device=dev)
@@ -117,9 +120,10 @@ class Workload:
 
     def step(self, i, ev=None):
         """One pass of the hot path on cache copy i.  The penalise-and-sample
-        passes of the decode steps run on a side stream (they are independent
-        of the attention) and join the main stream before the answer probe.
-        `ev` optionally collects HIP events on the main stream around the phases."""
+        pass over the logit rows of all decode steps (one call, row = token x
+        sequence) runs on a side stream, as it is independent of the
+        attention, and joins the main stream before the answer probe.  `ev`
+        optionally collects HIP events on the main stream around the phases."""
         wl = self.wl
         cache = B.KVCache(*self.copies[i])
         main = torch.cuda.current_stream()
@@ -134,10 +138,9 @@ class Workload:
             ev["c2"].record()
         self.side.wait_stream(main)
         with torch.cuda.stream(self.side):
-            for s in range(wl.decode_steps):
-                B.reco_penalty_sample(self.logits[s], self.refl, self.step_reward, TAU_LO, TAU_HI, *BETAS,
-                                      TEMPERATURE, SAMPLE_SEED, s, tokens=self.tokens[s], ws=self.ws_smp,
-                                      dev_err=self.dev_err)
+            B.reco_penalty_sample(self.logits.view(-1, self.logits.shape[-1]), self.refl, self.row_reward, TAU_LO,
+                                  TAU_HI, *BETAS, TEMPERATURE, SAMPLE_SEED, i, tokens=self.tokens, ws=self.ws_smp,
+                                  dev_err=self.dev_err)
         for s in range(wl.decode_steps):
             B.reco_decode_attn(cache, self.q[s], self.k_new[s], self.v_new[s], out=self.out, lse=self.lse,
                                ws=self.ws_dec, dev_err=self.dev_err)

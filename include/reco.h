@@ -12,6 +12,8 @@
  *   reco_score           window attention mass of every cached key   (Eq. 2)
  *   reco_select_compact  keep the top-m keys plus the window, compact
  *                        the K/V rows in place                       (Sec. 3.2)
+ *   reco_pool_scores     optional max / mean pooling of the prefix
+ *                        scores before selection (policy variant)    (Sec. 1)
  *   reco_decode_attn     GQA decode attention over the ragged,
  *                        compacted cache (optionally appending the
  *                        new token first)                            (Sec. 1, 3.2)
@@ -61,7 +63,7 @@
 extern "C" {
 #endif
 
-#define RECO_ABI_VERSION 2
+#define RECO_ABI_VERSION 3
 
 typedef enum reco_status {
   RECO_OK = 0,
@@ -111,18 +113,28 @@ typedef struct reco_kv_cache {
  * window and the group, for every j < L.  Entries j >= L are left untouched.
  *   q_win : [n_layers][batch][n_q_heads][w][head_dim], cache dtype
  *   scale : logit scale, normally 1/sqrt(head_dim)
+ *   row_stats : nullable [n_layers][batch][n_q_heads][w][2] fp32.  NULL: the
+ *           softmax normalisers of the window rows come from a first pass
+ *           over K (two passes in all).  Given: row t holds the (M, Z) pair
+ *           reco_decode_attn wrote when the token at position L - w + t was
+ *           decoded, and K is read once.  Exact (up to rounding) only when
+ *           no compression happened since the oldest window token was
+ *           decoded (the keys it saw then are keys 0..p now), with the same
+ *           scale; requires RECO_SCORE_CAUSAL.
  *   scores: [n_layers][batch][n_kv_heads][capacity] fp32 (output)
  * Requires 1 <= w <= capacity and G * w <= 4096.  Accumulation is fp32. */
 size_t reco_score_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers,
                                  int32_t n_q_heads, int32_t w);
 reco_status_t reco_score(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,
                          const void *q_win, int32_t n_q_heads, int32_t w, float scale,
-                         uint32_t flags, float *scores, void *ws, size_t ws_bytes,
+                         uint32_t flags, const float *row_stats, float *scores, void *ws,
+                         size_t ws_bytes,
                          int32_t *dev_err, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Section 3.2 (reward-driven retention and attention-guided selection):
- * per unit with L = len[unit], w_eff = min(w, L) and r = retention[seq],
+ * per unit with L = len[unit], w_eff = min(w, L) and
+ * r = retention[lc * retention_layer_stride + seq] (lc = layer - layer0),
  *   m = min(L, max(w_eff, ceil(r * L)))      (r * L as an IEEE fp64 product)
  * rows are kept: the window [L - w_eff, L) and the k = m - w_eff prefix
  * positions with the largest scores[unit][j] (ties: lower j first).  The kept
@@ -130,16 +142,38 @@ reco_status_t reco_score(const reco_kv_cache_t *cache, int32_t layer0, int32_t n
  * unit (bit-exact copies; rows >= m keep unspecified contents) and len is set
  * to m.
  *   scores    : [n_layers][batch][n_kv_heads][capacity] fp32, >= 0 (from reco_score)
- *   retention : [batch] fp64 in (0, 1]
+ *   retention : fp64 in (0, 1]; [batch] with retention_layer_stride = 0
+ *               (one retention level per sequence, as Section 3.2 sets it)
+ *               or [n_layers][batch] with stride = batch (per-layer
+ *               budgets, a policy variant; see reco_layer_retention)
  *   kept_idx  : nullable [n_layers][batch][n_kv_heads][capacity] int32 output;
  *               the first m entries of each unit receive the kept positions
  *               (ascending, in pre-compaction numbering)
  * A unit whose r or scores are invalid is left unchanged and dev_err is set. */
 size_t reco_select_compact_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers);
 reco_status_t reco_select_compact(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,
-                                  const float *scores, const double *retention, int32_t w,
-                                  int32_t *kept_idx, void *ws, size_t ws_bytes,
-                                  int32_t *dev_err, hipStream_t stream);
+                                  const float *scores, const double *retention,
+                                  int64_t retention_layer_stride, int32_t w, int32_t *kept_idx,
+                                  void *ws, size_t ws_bytes, int32_t *dev_err, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Score pooling before selection, a policy variant on the same kernels (the
+ * clustering idea of the eviction methods the paper cites, Section 1).  Per
+ * unit with L = len[unit] and prefix P = L - min(w, L):
+ *   pooled[j] = max  (mode RECO_POOL_MAX)  or
+ *               mean (mode RECO_POOL_MEAN) of scores[i] over the prefix
+ *               positions i with |i - j| <= kernel / 2,        for j < P
+ *   pooled[j] = scores[j]                                      for P <= j < L
+ * Entries at or beyond L are not written.  Means are summed in fp64 in index
+ * order and rounded to fp32 once; maxima are exact.
+ *   scores, pooled : [n_layers][batch][n_kv_heads][capacity] fp32, disjoint
+ *   kernel         : odd, 1 <= kernel <= 65 (1 copies the scores)
+ * A stored len outside [0, capacity] sets RECO_DEV_BAD_LENGTH (unit skipped). */
+#define RECO_POOL_MAX 0
+#define RECO_POOL_MEAN 1
+reco_status_t reco_pool_scores(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,
+                               int32_t w, const float *scores, float *pooled, int32_t kernel,
+                               int32_t mode, int32_t *dev_err, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Decode attention over the retained cache (the per-token attention cost of
@@ -155,6 +189,11 @@ reco_status_t reco_select_compact(const reco_kv_cache_t *cache, int32_t layer0, 
  *   k_new, v_new : both NULL (no append) or [n_layers][batch][n_kv_heads][head_dim]
  *   out          : [n_layers][batch][n_q_heads][head_dim], cache dtype (output)
  *   lse          : nullable [n_layers][batch][n_q_heads] fp32 (output)
+ *   row_stats    : nullable [n_layers][batch][n_q_heads][2] fp32 (output):
+ *                  (M, Z) with x_j = scale * log2(e) * <q, k_j>, M = max_j x_j
+ *                  and Z = sum_j 2^(x_j - M), so lse = (M + log2 Z) ln 2;
+ *                  kept for the window rows, they let reco_score skip its
+ *                  normaliser pass (empty: (-inf, 0))
  * An append with len == capacity is not performed (the token still takes part
  * in the attention) and sets RECO_DEV_APPEND_OVERFLOW. */
 size_t reco_decode_attn_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers,
@@ -162,7 +201,8 @@ size_t reco_decode_attn_workspace_size(const reco_kv_cache_t *cache, int32_t n_l
 reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,
                                const void *q, int32_t n_q_heads, float scale,
                                const void *k_new, const void *v_new, void *out, float *lse,
-                               void *ws, size_t ws_bytes, int32_t *dev_err, hipStream_t stream);
+                               float *row_stats, void *ws, size_t ws_bytes, int32_t *dev_err,
+                               hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Eq. 3 and Eq. 4 (Section 3.3, reward-banded reflection penalty): for every
@@ -231,6 +271,13 @@ reco_status_t reco_answer_ppl(const float *logits, const int32_t *tokens, int32_
  *   rewards are equal; NaN when n < 1 or v_hist is NULL. */
 double reco_retention_from_reward(double v, double lo, double hi);
 double reco_retention_eq1(const double *v_hist, int32_t n, double lambda, double delta);
+
+/* [host] Per-layer budgets (policy variant, the pyramid idea cited in
+ * Section 1): r_l = min(1, r * (1 + spread * (1 - 2 l / (n_layers - 1)))),
+ * a line falling with depth whose mean over layers is r (before the cap);
+ * r_l = r when n_layers = 1.  Evaluated in fp64 in exactly this order.  NaN
+ * unless 0 < r <= 1, 0 <= spread < 1 and 0 <= layer < n_layers. */
+double reco_layer_retention(double r, int32_t layer, int32_t n_layers, double spread);
 
 /* [host] The kept count of Section 3.2 that reco_select_compact uses:
  * m = min(L, max(min(w, L), ceil(r * L))) with r * L an IEEE fp64 product;

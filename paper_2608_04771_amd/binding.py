@@ -26,11 +26,14 @@ RECO_ERR_HIP = 4
 RECO_F32 = 0
 RECO_BF16 = 1
 RECO_SCORE_CAUSAL = 1
+RECO_POOL_MAX = 0
+RECO_POOL_MEAN = 1
 DEV_ERRORS = {0: "ok", 1: "append overflow", 2: "bad retention", 3: "bad score", 4: "bad token id",
               5: "bad length", 6: "bad logit row"}
 
 EXPORTED = [
     "reco_score_workspace_size", "reco_score", "reco_select_compact_workspace_size", "reco_select_compact",
+    "reco_pool_scores", "reco_layer_retention",
     "reco_decode_attn_workspace_size", "reco_decode_attn", "reco_logit_penalty",
     "reco_penalty_sample_workspace_size", "reco_penalty_sample",
     "reco_answer_ppl_workspace_size", "reco_answer_ppl", "reco_retention_from_reward", "reco_retention_eq1",
@@ -60,11 +63,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     C = ctypes.POINTER(RecoKVCache)
     sig = {
         "reco_score_workspace_size": (SZ, [C, I32, I32, I32]),
-        "reco_score": (I32, [C, I32, I32, P, I32, I32, F32, U32, P, P, SZ, P, P]),
+        "reco_score": (I32, [C, I32, I32, P, I32, I32, F32, U32, P, P, P, SZ, P, P]),
         "reco_select_compact_workspace_size": (SZ, [C, I32]),
-        "reco_select_compact": (I32, [C, I32, I32, P, P, I32, P, P, SZ, P, P]),
+        "reco_select_compact": (I32, [C, I32, I32, P, P, I64, I32, P, P, SZ, P, P]),
+        "reco_pool_scores": (I32, [C, I32, I32, I32, P, P, I32, I32, P, P]),
+        "reco_layer_retention": (F64, [F64, I32, I32, F64]),
         "reco_decode_attn_workspace_size": (SZ, [C, I32, I32]),
-        "reco_decode_attn": (I32, [C, I32, I32, P, I32, F32, P, P, P, P, P, SZ, P, P]),
+        "reco_decode_attn": (I32, [C, I32, I32, P, I32, F32, P, P, P, P, P, P, SZ, P, P]),
         "reco_logit_penalty": (I32, [P, I32, I32, I64, P, I32, P, F32, F32, F32, F32, F32, P, P]),
         "reco_penalty_sample_workspace_size": (SZ, [I32, I32]),
         "reco_penalty_sample": (I32, [P, I32, I32, I64, P, I32, P, F32, F32, F32, F32, F32, F32, U64, U64, P, P, SZ,
@@ -174,8 +179,11 @@ def decode_workspace(cache: "KVCache", n_q_heads: int, n_layers: Optional[int] =
 
 def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[float] = None, causal: bool = True,
                scores: Optional[torch.Tensor] = None, layer0: int = 0, n_layers: Optional[int] = None,
-               ws: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Eq. 2 window attention mass; returns scores [NL][B][H][Cap] fp32."""
+               ws: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None,
+               row_stats: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Eq. 2 window attention mass; returns scores [NL][B][H][Cap] fp32.
+    ``row_stats`` ([n_layers][B][Hq][w][2], from the window tokens' decode
+    steps) replaces the normaliser pass over K."""
     layer0, nl = _layers(cache, layer0, n_layers)
     NL, B, H, Cap, D = cache.shape
     if q_win.dim() != 5 or q_win.shape[0] != nl or q_win.shape[1] != B or q_win.shape[3] != w or q_win.shape[4] != D:
@@ -185,11 +193,14 @@ def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[floa
     hq = q_win.shape[2]
     if scores is None:
         scores = torch.zeros((nl, B, H, Cap), dtype=torch.float32, device=cache.k.device)
-    _need_cuda(q_win, scores, ws, dev_err)
+    if row_stats is not None and (row_stats.dtype != torch.float32 or tuple(row_stats.shape) != (nl, B, hq, w, 2)):
+        raise ValueError("row_stats must be float32 [n_layers][B][Hq][w][2]")
+    _need_cuda(q_win, scores, ws, dev_err, row_stats)
     ws = _ws(score_workspace_size(cache, hq, w, nl), cache.k.device, ws)
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     st = load_library().reco_score(cache.ref(), layer0, nl, _ptr(q_win), hq, w, scale,
-                                   RECO_SCORE_CAUSAL if causal else 0, _ptr(scores), _ptr(ws), ws.numel(),
+                                   RECO_SCORE_CAUSAL if causal else 0, _ptr(row_stats), _ptr(scores), _ptr(ws),
+                                   ws.numel(),
                                    _ptr(dev_err), _stream(cache.k.device))
     _check(st, "reco_score")
     return scores
@@ -198,29 +209,60 @@ def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[floa
 def reco_select_compact(cache: KVCache, scores: torch.Tensor, retention: torch.Tensor, w: int,
                         kept_idx: Optional[torch.Tensor] = None, layer0: int = 0, n_layers: Optional[int] = None,
                         ws: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None):
-    """Select the reward budget per unit and compact K/V in place (len <- m)."""
+    """Select the reward budget per unit and compact K/V in place (len <- m).
+    ``retention`` is float64 [B] (one level per sequence) or [n_layers][B]
+    (per-layer budgets)."""
     layer0, nl = _layers(cache, layer0, n_layers)
-    if retention.dtype != torch.float64 or retention.numel() != cache.shape[1]:
-        raise ValueError("retention must be float64 [B]")
+    Bsz = cache.shape[1]
+    if retention.dtype != torch.float64:
+        raise ValueError("retention must be float64")
+    if tuple(retention.shape) == (Bsz,):
+        stride = 0
+    elif tuple(retention.shape) == (nl, Bsz):
+        stride = Bsz
+    else:
+        raise ValueError("retention must be [B] or [n_layers][B]")
     if scores.dtype != torch.float32:
         raise ValueError("scores must be float32")
     if kept_idx is not None and kept_idx.dtype != torch.int32:
         raise ValueError("kept_idx must be int32")
     _need_cuda(scores, retention, kept_idx, ws, dev_err)
     ws = _ws(select_compact_workspace_size(cache, nl), cache.k.device, ws)
-    st = load_library().reco_select_compact(cache.ref(), layer0, nl, _ptr(scores), _ptr(retention), w,
+    st = load_library().reco_select_compact(cache.ref(), layer0, nl, _ptr(scores), _ptr(retention), stride, w,
                                             _ptr(kept_idx), _ptr(ws), ws.numel(), _ptr(dev_err),
                                             _stream(cache.k.device))
     _check(st, "reco_select_compact")
     return kept_idx
 
 
+def reco_pool_scores(cache: KVCache, scores: torch.Tensor, w: int, kernel: int, mode: str = "max",
+                     pooled: Optional[torch.Tensor] = None, layer0: int = 0, n_layers: Optional[int] = None,
+                     dev_err: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Max / mean pooling of the prefix scores (window scores copied); returns
+    pooled [n_layers][B][H][Cap] fp32 (entries at or beyond len unwritten)."""
+    layer0, nl = _layers(cache, layer0, n_layers)
+    if scores.dtype != torch.float32:
+        raise ValueError("scores must be float32")
+    if mode not in ("max", "mean"):
+        raise ValueError("mode must be 'max' or 'mean'")
+    if pooled is None:
+        pooled = torch.zeros_like(scores)
+    _need_cuda(scores, pooled, dev_err)
+    st = load_library().reco_pool_scores(cache.ref(), layer0, nl, w, _ptr(scores), _ptr(pooled), kernel,
+                                         RECO_POOL_MAX if mode == "max" else RECO_POOL_MEAN, _ptr(dev_err),
+                                         _stream(cache.k.device))
+    _check(st, "reco_pool_scores")
+    return pooled
+
+
 def reco_decode_attn(cache: KVCache, q: torch.Tensor, k_new: Optional[torch.Tensor] = None,
                      v_new: Optional[torch.Tensor] = None, scale: Optional[float] = None,
                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None, want_lse: bool = True,
                      layer0: int = 0, n_layers: Optional[int] = None, ws: Optional[torch.Tensor] = None,
-                     dev_err: Optional[torch.Tensor] = None):
-    """GQA decode attention (optionally appending the new token); returns (out, lse)."""
+                     dev_err: Optional[torch.Tensor] = None, row_stats: Optional[torch.Tensor] = None):
+    """GQA decode attention (optionally appending the new token); returns (out, lse).
+    ``row_stats`` ([n_layers][B][Hq][2] fp32) optionally receives each query's
+    (max, sum) of the log2-domain logits."""
     layer0, nl = _layers(cache, layer0, n_layers)
     NL, B, H, Cap, D = cache.shape
     if q.dim() != 4 or q.shape[0] != nl or q.shape[1] != B or q.shape[3] != D or q.dtype != cache.k.dtype:
@@ -230,11 +272,13 @@ def reco_decode_attn(cache: KVCache, q: torch.Tensor, k_new: Optional[torch.Tens
         out = torch.empty_like(q)
     if lse is None and want_lse:
         lse = torch.empty((nl, B, hq), dtype=torch.float32, device=q.device)
-    _need_cuda(q, k_new, v_new, out, lse, ws, dev_err)
+    if row_stats is not None and (row_stats.dtype != torch.float32 or tuple(row_stats.shape) != (nl, B, hq, 2)):
+        raise ValueError("row_stats must be float32 [n_layers][B][Hq][2]")
+    _need_cuda(q, k_new, v_new, out, lse, ws, dev_err, row_stats)
     ws = _ws(decode_attn_workspace_size(cache, hq, nl), q.device, ws)
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     st = load_library().reco_decode_attn(cache.ref(), layer0, nl, _ptr(q), hq, scale, _ptr(k_new), _ptr(v_new),
-                                         _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _ptr(dev_err),
+                                         _ptr(out), _ptr(lse), _ptr(row_stats), _ptr(ws), ws.numel(), _ptr(dev_err),
                                          _stream(q.device))
     _check(st, "reco_decode_attn")
     return out, lse
@@ -315,6 +359,10 @@ def reco_retention_from_reward(v: float, lo: float = 0.3, hi: float = 1.0) -> fl
 def reco_retention_eq1(v_hist: Sequence[float], lam: float = 0.25, delta: float = 0.1) -> float:
     arr = (ctypes.c_double * len(v_hist))(*[float(x) for x in v_hist])
     return float(load_library().reco_retention_eq1(arr, len(v_hist), float(lam), float(delta)))
+
+
+def reco_layer_retention(r: float, layer: int, n_layers: int, spread: float) -> float:
+    return float(load_library().reco_layer_retention(float(r), int(layer), int(n_layers), float(spread)))
 
 
 def reco_kept_count(L: int, w: int, r: float) -> int:

@@ -18,7 +18,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libreco.so")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["decode_attn.hip", "score.hip", "select_compact.hip", "logits.hip"]
+HIP_SOURCES = ["decode_attn.hip", "score.hip", "select_compact.hip", "pool_scores.hip", "logits.hip"]
 HOST_SOURCES = ["abi.cpp"]
 
 # Packed fp32 instructions are kept out of every kernel (v_pk_* fp32 forms).
@@ -52,7 +52,9 @@ def build_library(verbose: bool = False) -> str:
                            "-c", os.path.join(CSRC, src), "-o", obj]))
     for src in HOST_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
-        jobs.append((obj, [hipcc, f"--offload-arch={ARCH}", *common, "-c", os.path.join(CSRC, src), "-o", obj]))
+        # fp64 host policies are computed without contraction, as the formulas are written
+        jobs.append((obj, [hipcc, f"--offload-arch={ARCH}", *common, "-ffp-contract=off", "-c",
+                           os.path.join(CSRC, src), "-o", obj]))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
         outs = list(ex.map(lambda j: _run(j[1]), jobs))
     if verbose:

@@ -13,6 +13,17 @@ The paper's loop, per completed reasoning step i with process reward v_i:
 * two consecutive top-band rewards trigger the answer probe, whose
   perplexity decides the stop (Eq. 5-6).
 
+Scoring reuses the softmax statistics that decode attention wrote for the
+window tokens (one pass over K instead of two) whenever every window token
+was decoded after the last compression, so that the keys each of them saw
+are exactly the keys it sees now.
+
+Policy variants on the same kernels: delta = 0 (one uniform retention, the
+paper's own ablation of Eq. 1), per-layer budgets (`layer_spread`, a
+retention falling linearly with depth that averages r) and pooled scores
+(`pool_kernel`, max or mean pooling of the prefix scores before the top-k),
+the last two after the eviction methods the paper cites in Section 1.
+
 `RewardSchedule` holds the pure host bookkeeping (reward history, retention,
 compression trigger, probe trigger) and runs without a GPU.  `RecoDecoder`
 drives the kernels through the binding: it keeps the window queries in a ring
@@ -47,19 +58,30 @@ class RecoPolicy:
     tau_hi: float = 0.8
     tau_p: float = 1.1
     betas: Sequence[float] = (0.0, 1.0, 3.0)   # penalty in the low / middle / high band
+    layer_spread: float = 0.0        # per-layer budgets: r_l from r(1 + spread) at layer 0 to r(1 - spread)
+    pool_kernel: int = 1             # score pooling before selection (1: none; odd, <= 65)
+    pool_mode: str = "max"           # "max" | "mean"
+    stats_fed: bool = True           # score with the window tokens' decode statistics when they are exact
 
 
 class RewardSchedule:
-    """Per-sequence host state: reward history, cache length bookkeeping and
-    the two triggers.  Lengths follow the same fp64 kept-count rule as the
-    select kernel, so no device read-back is needed."""
+    """Per-sequence host state: reward history, cache length bookkeeping (one
+    length per layer) and the two triggers.  Lengths follow the same fp64
+    kept-count rule as the select kernel, so no device read-back is needed."""
 
-    def __init__(self, policy: RecoPolicy, prompt_len: int):
+    def __init__(self, policy: RecoPolicy, prompt_len: int, n_layers: int = 1):
         self.policy = policy
+        self.n_layers = int(n_layers)
         self.rewards: List[float] = []
-        self.length = int(prompt_len)          # L: current cache length
-        self.length_at_compress = int(prompt_len)   # L_{i-1} (the prompt length at first)
+        self.lengths = [int(prompt_len)] * self.n_layers   # L per layer
+        self.length_at_compress = int(prompt_len)          # layer 0's L after the last compression
+        self.grown = 0                                     # tokens appended since the last compression
         self.top_streak = 0
+
+    @property
+    def length(self) -> int:
+        """Layer 0's cache length (every layer's when the budget is uniform)."""
+        return self.lengths[0]
 
     def retention(self) -> float:
         p = self.policy
@@ -68,8 +90,15 @@ class RewardSchedule:
             return B.reco_retention_from_reward(v, p.lo, p.hi)
         return B.reco_retention_eq1(self.rewards, p.lam, p.delta)
 
+    def layer_retentions(self, r: float) -> List[float]:
+        """The retention of every layer for sequence-level retention r."""
+        if self.policy.layer_spread == 0.0:
+            return [r] * self.n_layers
+        return [B.reco_layer_retention(r, l, self.n_layers, self.policy.layer_spread) for l in range(self.n_layers)]
+
     def token_appended(self, n: int = 1):
-        self.length += n
+        self.lengths = [L + n for L in self.lengths]
+        self.grown += n
 
     def end_step(self, reward: float):
         """Record v_i.  Returns (compress, r, probe): whether the cache is due
@@ -79,13 +108,15 @@ class RewardSchedule:
         p = self.policy
         self.top_streak = self.top_streak + 1 if reward >= p.tau_hi else 0
         probe = self.top_streak >= 2
-        compress = self.length - self.length_at_compress >= max(1, p.interval)
+        compress = self.grown >= max(1, p.interval)
         r = self.retention()
         return compress, r, probe
 
     def compressed(self, r: float):
-        self.length = B.reco_kept_count(self.length, self.policy.window, r)
-        self.length_at_compress = self.length
+        w = self.policy.window
+        self.lengths = [B.reco_kept_count(L, w, rl) for L, rl in zip(self.lengths, self.layer_retentions(r))]
+        self.length_at_compress = self.lengths[0]
+        self.grown = 0
 
 
 class RecoDecoder:
@@ -108,8 +139,11 @@ class RecoDecoder:
         self.cache, self.policy, self.hq = cache, policy, n_q_heads
         dev = cache.k.device
         prompt_len = int(cache.length[0, 0, 0].item())
-        self.sched = [RewardSchedule(policy, prompt_len) for _ in range(Bsz)]
+        self.sched = [RewardSchedule(policy, prompt_len, NL) for _ in range(Bsz)]
         self.ring = prompt_q.clone()                      # row t % w holds the query of token t
+        # slot t % w holds the (max, sum) decode statistics of token t, [w][NL][B][Hq][2]
+        self.stats_ring = torch.zeros((w, NL, Bsz, n_q_heads, 2), dtype=torch.float32, device=dev)
+        self.last_score_stats_fed = False
         self.count = prompt_len                           # tokens seen (absolute position of the next one)
         self.refl = refl_ids
         self.band_reward = torch.zeros(Bsz, dtype=torch.float32, device=dev)   # no penalty before the first reward
@@ -118,7 +152,9 @@ class RecoDecoder:
         self.ws_sel = torch.empty(B.select_compact_workspace_size(cache), dtype=torch.uint8, device=dev)
         self.scores = torch.zeros((NL, Bsz, H, Cap), dtype=torch.float32, device=dev)
         self.kept = torch.zeros((NL, Bsz, H, Cap), dtype=torch.int32, device=dev) if record_kept else None
-        self.retention = torch.ones(Bsz, dtype=torch.float64, device=dev)
+        per_layer = policy.layer_spread != 0.0
+        self.retention = torch.ones((NL, Bsz) if per_layer else (Bsz,), dtype=torch.float64, device=dev)
+        self.pooled = torch.zeros_like(self.scores) if policy.pool_kernel > 1 else None
         self.dev_err = torch.zeros(1, dtype=torch.int32, device=dev)
         self.out = torch.empty((NL, Bsz, n_q_heads, D), dtype=cache.k.dtype, device=dev)
         self.lse = torch.empty((NL, Bsz, n_q_heads), dtype=torch.float32, device=dev)
@@ -139,7 +175,7 @@ class RecoDecoder:
         w = self.policy.window
         self.ring[:, :, :, self.count % w, :].copy_(q)
         B.reco_decode_attn(self.cache, q, k_new, v_new, out=self.out, lse=self.lse, ws=self.ws_dec,
-                           dev_err=self.dev_err)
+                           dev_err=self.dev_err, row_stats=self.stats_ring[self.count % w])
         if logits is not None and self.refl is not None:
             p = self.policy
             B.reco_logit_penalty(logits, self.refl, self.band_reward, p.tau_lo, p.tau_hi, *p.betas,
@@ -170,6 +206,11 @@ class RecoDecoder:
         w = self.policy.window
         return torch.roll(self.ring, shifts=-(self.count % w), dims=3).contiguous()
 
+    def window_stats(self) -> torch.Tensor:
+        """Decode statistics of the last w tokens in order, [NL][B][Hq][w][2]."""
+        w = self.policy.window
+        return torch.roll(self.stats_ring, shifts=-(self.count % w), dims=0).permute(1, 2, 3, 0, 4).contiguous()
+
     def end_step(self, rewards: Sequence[float]):
         """A reasoning step ended with process rewards v (one per sequence).
         Compresses when due and updates the penalty band for the next step.
@@ -180,12 +221,25 @@ class RecoDecoder:
         due = [d[0] for d in decisions]
         if not any(due):
             return False, probe
-        # Sequences not due keep everything (r = 1 keeps every row in place).
+        # Sequences not due keep everything (r = 1 in every layer keeps every row in place).
         r = [d[1] if d[0] else 1.0 for d in decisions]
-        self.retention.copy_(torch.tensor(r, dtype=torch.float64))
-        B.reco_score(self.cache, self.window_queries(), self.policy.window, scores=self.scores, ws=self.ws_score,
-                     dev_err=self.dev_err)
-        B.reco_select_compact(self.cache, self.scores, self.retention, self.policy.window, kept_idx=self.kept,
+        if self.retention.dim() == 2:
+            cols = [s.layer_retentions(rr) if d else [1.0] * s.n_layers for s, d, rr in zip(self.sched, due, r)]
+            self.retention.copy_(torch.tensor(cols, dtype=torch.float64).T)
+        else:
+            self.retention.copy_(torch.tensor(r, dtype=torch.float64))
+        p = self.policy
+        # Decode statistics are exact normalisers only if no compression happened
+        # since the oldest window token was decoded.
+        fed = p.stats_fed and all(sc.grown >= p.window for sc in self.sched)
+        self.last_score_stats_fed = fed
+        B.reco_score(self.cache, self.window_queries(), p.window, scores=self.scores, ws=self.ws_score,
+                     dev_err=self.dev_err, row_stats=self.window_stats() if fed else None)
+        ranked = self.scores
+        if self.pooled is not None:
+            ranked = B.reco_pool_scores(self.cache, self.scores, p.window, p.pool_kernel, p.pool_mode,
+                                        pooled=self.pooled, dev_err=self.dev_err)
+        B.reco_select_compact(self.cache, ranked, self.retention, p.window, kept_idx=self.kept,
                               ws=self.ws_sel, dev_err=self.dev_err)
         for s, d, rr in zip(self.sched, due, r):
             if d:
@@ -197,4 +251,9 @@ class RecoDecoder:
         return B.reco_answer_ppl(logits, tokens, self.policy.tau_p, dev_err=self.dev_err)
 
     def lengths(self) -> List[int]:
+        """Layer 0's cache length of every sequence."""
         return [s.length for s in self.sched]
+
+    def layer_lengths(self) -> List[List[int]]:
+        """[B][NL] cache lengths."""
+        return [list(s.lengths) for s in self.sched]

@@ -77,6 +77,16 @@ double reco_retention_eq1(const double *v_hist, int32_t n, double lambda, double
   return lambda - delta * (v_hist[n - 1] - mean) / (vmax - vmin);
 }
 
+double reco_layer_retention(double r, int32_t layer, int32_t n_layers, double spread) {
+  if (!(r > 0.0 && r <= 1.0) || !(spread >= 0.0 && spread < 1.0) || n_layers < 1 || layer < 0 ||
+      layer >= n_layers)
+    return NAN;
+  if (n_layers == 1) return r;
+  const double t = static_cast<double>(layer) / static_cast<double>(n_layers - 1);
+  const double x = r * (1.0 + spread * (1.0 - 2.0 * t));
+  return x < 1.0 ? x : 1.0;
+}
+
 int32_t reco_kept_count(int32_t L, int32_t w, double r) {
   if (!(r > 0.0 && r <= 1.0) || L < 0 || w < 1) return -1;
   const int32_t w_eff = w < L ? w : L;
@@ -96,9 +106,10 @@ size_t reco_score_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers,
 }
 
 reco_status_t reco_score(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers, const void *q_win,
-                         int32_t n_q_heads, int32_t w, float scale, uint32_t flags, float *scores, void *ws,
-                         size_t ws_bytes, int32_t *dev_err, hipStream_t stream) {
+                         int32_t n_q_heads, int32_t w, float scale, uint32_t flags, const float *row_stats,
+                         float *scores, void *ws, size_t ws_bytes, int32_t *dev_err, hipStream_t stream) {
   if (!cache_ok(cache) || !q_win || !scores) return RECO_ERR_INVALID_ARG;
+  if (row_stats && !(flags & RECO_SCORE_CAUSAL)) return RECO_ERR_INVALID_ARG;   // decode statistics are causal
   if (!layers_ok(cache, layer0, n_layers) || !units_ok(cache, n_layers)) return RECO_ERR_INVALID_ARG;
   if (w < 1 || w > cache->capacity || !isfinite(scale) || (flags & ~RECO_SCORE_CAUSAL)) return RECO_ERR_INVALID_ARG;
   const int G = group_of(cache, n_q_heads);
@@ -120,6 +131,7 @@ reco_status_t reco_score(const reco_kv_cache_t *cache, int32_t layer0, int32_t n
   p.chunks = (cache->capacity + reco::kScoreChunk - 1) / reco::kScoreChunk;
   p.row_part = reinterpret_cast<float *>(ws);
   p.row_stat = p.row_part + static_cast<size_t>(units) * p.chunks * p.rows_pad * 2;
+  p.given = row_stats;
   p.dev_err = dev_err;
   p.layer0 = layer0;
   p.n_layers = n_layers;
@@ -142,9 +154,10 @@ size_t reco_select_compact_workspace_size(const reco_kv_cache_t *cache, int32_t 
 }
 
 reco_status_t reco_select_compact(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,
-                                  const float *scores, const double *retention, int32_t w, int32_t *kept_idx,
-                                  void *ws, size_t ws_bytes, int32_t *dev_err, hipStream_t stream) {
-  if (!cache_ok(cache) || !scores || !retention) return RECO_ERR_INVALID_ARG;
+                                  const float *scores, const double *retention, int64_t retention_layer_stride,
+                                  int32_t w, int32_t *kept_idx, void *ws, size_t ws_bytes, int32_t *dev_err,
+                                  hipStream_t stream) {
+  if (!cache_ok(cache) || !scores || !retention || retention_layer_stride < 0) return RECO_ERR_INVALID_ARG;
   if (!layers_ok(cache, layer0, n_layers) || !units_ok(cache, n_layers)) return RECO_ERR_INVALID_ARG;
   if (w < 1 || w > cache->capacity) return RECO_ERR_INVALID_ARG;
   reco_status_t st = cache_supported(cache);
@@ -159,6 +172,7 @@ reco_status_t reco_select_compact(const reco_kv_cache_t *cache, int32_t layer0, 
   p.len = cache->len;
   p.scores = scores;
   p.retention = retention;
+  p.ret_stride = retention_layer_stride;
   p.kept = reinterpret_cast<int32_t *>(ws);
   const size_t kept_bytes = (static_cast<size_t>(units) * sizeof(int32_t) + 255) / 256 * 256;
   p.idx = kept_idx ? kept_idx : reinterpret_cast<int32_t *>(reinterpret_cast<char *>(ws) + kept_bytes);
@@ -172,6 +186,34 @@ reco_status_t reco_select_compact(const reco_kv_cache_t *cache, int32_t layer0, 
   return hip_status(reco::launch_select_compact(p, cache->dtype, cache->head_dim, stream));
 }
 
+// ---------------------------------------------------------------- pooling
+reco_status_t reco_pool_scores(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers, int32_t w,
+                               const float *scores, float *pooled, int32_t kernel, int32_t mode, int32_t *dev_err,
+                               hipStream_t stream) {
+  if (!cache_ok(cache) || !scores || !pooled) return RECO_ERR_INVALID_ARG;
+  if (!layers_ok(cache, layer0, n_layers) || !units_ok(cache, n_layers)) return RECO_ERR_INVALID_ARG;
+  if (w < 1 || w > cache->capacity) return RECO_ERR_INVALID_ARG;
+  if (kernel < 1 || kernel > reco::kPoolMaxKernel || kernel % 2 == 0) return RECO_ERR_INVALID_ARG;
+  if (mode != RECO_POOL_MAX && mode != RECO_POOL_MEAN) return RECO_ERR_INVALID_ARG;
+  const size_t bytes = static_cast<size_t>(n_layers) * cache->batch * cache->n_kv_heads * cache->capacity * 4;
+  const char *a = reinterpret_cast<const char *>(scores), *o = reinterpret_cast<const char *>(pooled);
+  if (a < o + bytes && o < a + bytes) return RECO_ERR_INVALID_ARG;     // in and out must not overlap
+  reco::PoolParams p{};
+  p.len = cache->len;
+  p.scores = scores;
+  p.pooled = pooled;
+  p.dev_err = dev_err;
+  p.layer0 = layer0;
+  p.n_layers = n_layers;
+  p.batch = cache->batch;
+  p.hkv = cache->n_kv_heads;
+  p.cap = cache->capacity;
+  p.w = w;
+  p.kernel = kernel;
+  p.mode = mode;
+  return hip_status(reco::launch_pool_scores(p, stream));
+}
+
 // ---------------------------------------------------------------- decode
 size_t reco_decode_attn_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers, int32_t n_q_heads) {
   if (!cache_ok(cache) || n_layers < 1 || group_of(cache, n_q_heads) < 1) return 0;
@@ -181,7 +223,8 @@ size_t reco_decode_attn_workspace_size(const reco_kv_cache_t *cache, int32_t n_l
 
 reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers, const void *q,
                                int32_t n_q_heads, float scale, const void *k_new, const void *v_new, void *out,
-                               float *lse, void *ws, size_t ws_bytes, int32_t *dev_err, hipStream_t stream) {
+                               float *lse, float *row_stats, void *ws, size_t ws_bytes, int32_t *dev_err,
+                               hipStream_t stream) {
   if (!cache_ok(cache) || !q || !out) return RECO_ERR_INVALID_ARG;
   if ((k_new == nullptr) != (v_new == nullptr)) return RECO_ERR_INVALID_ARG;
   if (!layers_ok(cache, layer0, n_layers) || !units_ok(cache, n_layers) || !isfinite(scale))
@@ -204,6 +247,7 @@ reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int
   p.v_new = v_new;
   p.out = out;
   p.lse = lse;
+  p.row_stats = row_stats;
   p.splits = reco::decode_splits(units, cache->capacity);
   p.part_o = reinterpret_cast<float *>(ws);
   p.part_ml = p.part_o + static_cast<size_t>(units) * p.splits * 16 * cache->head_dim;

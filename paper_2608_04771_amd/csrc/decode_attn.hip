@@ -387,9 +387,12 @@ __global__ __launch_bounds__(kWave) void decode_merge_kernel(DecodeParams p) {
   T *out = reinterpret_cast<T *>(p.out) + ((static_cast<size_t>(lc) * p.batch + b) * p.hq + h * p.group + qi) * D;
 #pragma unroll
   for (int i = 0; i < kPer; ++i) out[lane + i * kWave] = from_f32<T>(acc[i]);
-  if (p.lse && lane == 0)
-    p.lse[(static_cast<size_t>(lc) * p.batch + b) * p.hq + h * p.group + qi] =
-        L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+  const size_t oq = (static_cast<size_t>(lc) * p.batch + b) * p.hq + h * p.group + qi;
+  if (p.lse && lane == 0) p.lse[oq] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+  if (p.row_stats && lane == 0) {
+    p.row_stats[oq * 2 + 0] = M;
+    p.row_stats[oq * 2 + 1] = L;
+  }
 
   if (qi != 0) return;
   if (lane == 0 && (len_in < 0 || len_in > p.cap)) report(p.dev_err, 5 /*RECO_DEV_BAD_LENGTH*/);

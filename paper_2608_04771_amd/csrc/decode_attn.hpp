@@ -18,6 +18,7 @@ struct DecodeParams {
   const void *v_new;
   void *out;              // [n_layers][batch][hq][D]
   float *lse;             // nullable [n_layers][batch][hq]
+  float *row_stats;       // nullable [n_layers][batch][hq][2]: (max, sum) of the log2-domain logits
   float *part_o;          // [units][splits][16][D]
   float *part_ml;         // [units][splits][32]  (16 maxima, 16 sums)
   int32_t *dev_err;

@@ -18,6 +18,7 @@ struct ScoreParams {
   float *scores;          // [n_layers][batch][hkv][cap]
   float *row_part;        // [units][chunks][rows_pad][2]  per-chunk (max, sum) in log2 domain
   float *row_stat;        // [units][rows_pad][2]          (max, 1/sum)
+  const float *given;     // nullable [n_layers][batch][hq][w][2] window-row (max, sum) from decode
   int32_t *dev_err;
   int layer0, n_layers, batch, hkv, cap, group, hq, w, rows, rows_pad, chunks;
   int causal;
@@ -34,14 +35,26 @@ struct SelectParams {
   void *v;
   int32_t *len;
   const float *scores;    // [n_layers][batch][hkv][cap]
-  const double *retention;  // [batch]
+  const double *retention;  // [batch], or [n_layers][batch] with ret_stride = batch
   int32_t *idx;           // [n_layers][batch][hkv][cap]  kept positions (user buffer or workspace)
   int32_t *kept;          // [units] kept count m, or -1 for "leave unchanged"
   int32_t *dev_err;
+  int64_t ret_stride;     // retention of (covered layer lc, seq b) = retention[lc * ret_stride + b]
   int layer0, n_layers, batch, hkv, cap, w;
 };
 size_t select_workspace_bytes(int units, int capacity, bool need_idx);
 hipError_t launch_select_compact(const SelectParams &p, int dtype, int head_dim, hipStream_t s);
+
+// ---- score pooling (policy variant) ---------------------------------------------
+constexpr int kPoolMaxKernel = 65;
+struct PoolParams {
+  const int32_t *len;
+  const float *scores;    // [n_layers][batch][hkv][cap]
+  float *pooled;          // same shape, must not overlap scores
+  int32_t *dev_err;
+  int layer0, n_layers, batch, hkv, cap, w, kernel, mode;
+};
+hipError_t launch_pool_scores(const PoolParams &p, hipStream_t s);
 
 // ---- reflection penalty ------------------------------------------------------
 hipError_t launch_logit_penalty(float *logits, int rows, int vocab, int64_t ld, const int32_t *ids,

@@ -367,15 +367,47 @@ __global__ __launch_bounds__(kThreads) void score_rowmerge_kernel(ScoreParams p)
   dst[1] = ok ? static_cast<float>(1.0 / Z) : 0.f;
 }
 
+// Row normalisers taken from the decode steps of the window tokens: the
+// (max, sum) pair decode wrote for query head g at position L - w + t is row
+// g * w + t's statistic; absent or empty rows get (+inf, 0) as above.
+__global__ __launch_bounds__(kThreads) void score_given_stats_kernel(ScoreParams p) {
+  const UnitInfo u = unit_info(p, blockIdx.y);
+  const int r = blockIdx.x * kThreads + threadIdx.x;
+  if (r >= p.rows_pad) return;
+  const int g = r / p.w;
+  const int t = r - g * p.w;
+  const bool valid = r < p.rows && u.L - p.w + t >= 0;
+  float M = INFINITY, Z = 0.f;
+  if (valid) {
+    const float *src =
+        p.given + ((((static_cast<size_t>(u.lc) * p.batch + u.b) * p.hq + u.h * p.group + g) * p.w) + t) * 2;
+    M = src[0];
+    Z = src[1];
+  }
+  const bool ok = valid && M != -INFINITY && M != INFINITY && Z > 0.f;
+  float *dst = p.row_stat + (u.ounit * p.rows_pad + r) * 2;
+  dst[0] = ok ? M : INFINITY;
+  dst[1] = ok ? 1.f / Z : 0.f;
+}
+
 template <typename T, int D, int RTW>
 hipError_t launch_rtw(const ScoreParams &p, int waves, hipStream_t s) {
   const int units = p.n_layers * p.batch * p.hkv;
-  hipLaunchKernelGGL((score_stats_kernel<T, D, RTW>), dim3(p.chunks, units), dim3(waves * kWave), 0, s, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(score_rowmerge_kernel, dim3((p.rows_pad + kThreads - 1) / kThreads, units), dim3(kThreads), 0, s, p);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e;
+  if (p.given) {
+    hipLaunchKernelGGL(score_given_stats_kernel, dim3((p.rows_pad + kThreads - 1) / kThreads, units), dim3(kThreads),
+                       0, s, p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  } else {
+    hipLaunchKernelGGL((score_stats_kernel<T, D, RTW>), dim3(p.chunks, units), dim3(waves * kWave), 0, s, p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(score_rowmerge_kernel, dim3((p.rows_pad + kThreads - 1) / kThreads, units), dim3(kThreads), 0,
+                       s, p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL((score_mass_kernel<T, D, RTW>), dim3(p.chunks, units), dim3(waves * kWave), 0, s, p);
   return hipGetLastError();
 }

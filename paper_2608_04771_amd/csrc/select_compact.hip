@@ -86,7 +86,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
   const int tid = threadIdx.x;
 
   const int L = p.len[cunit];
-  const double r = p.retention[b];
+  const double r = p.retention[static_cast<int64_t>(lc) * p.ret_stride + b];
   if (L < 0 || L > p.cap) {
     if (tid == 0) {
       report(p.dev_err, 5 /*RECO_DEV_BAD_LENGTH*/);

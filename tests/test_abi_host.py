@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     lib = B.load_library()
-    assert B.reco_abi_version() == 2
+    assert B.reco_abi_version() == 3
     assert lib.reco_status_str(0) == b"ok"
     assert b"workspace" in lib.reco_status_str(3)
     assert lib.reco_status_str(99) == b"unknown status"
@@ -73,9 +73,10 @@ def _fake_cache(**kw):
 P = ctypes.c_void_p
 
 
-def _score(c, layer0=0, nl=2, q=0x10, hq=4, w=8, scale=0.1, flags=1, scores=0x20, ws=0x30, wsb=1 << 30):
+def _score(c, layer0=0, nl=2, q=0x10, hq=4, w=8, scale=0.1, flags=1, stats=0, scores=0x20, ws=0x30, wsb=1 << 30):
     lib = B.load_library()
-    return lib.reco_score(ctypes.byref(c), layer0, nl, P(q), hq, w, scale, flags, P(scores), P(ws), wsb, None, None)
+    return lib.reco_score(ctypes.byref(c), layer0, nl, P(q), hq, w, scale, flags, P(stats) if stats else None,
+                          P(scores), P(ws), wsb, None, None)
 
 
 def test_score_rejects_bad_arguments():
@@ -90,6 +91,7 @@ def test_score_rejects_bad_arguments():
     assert _score(ok, w=65) == B.RECO_ERR_INVALID_ARG                    # window beyond capacity
     assert _score(ok, scale=float("nan")) == B.RECO_ERR_INVALID_ARG
     assert _score(ok, flags=2) == B.RECO_ERR_INVALID_ARG
+    assert _score(ok, flags=0, stats=0x70) == B.RECO_ERR_INVALID_ARG      # decode statistics are causal
     assert _score(_fake_cache(head_dim=96)) == B.RECO_ERR_UNSUPPORTED
     assert _score(_fake_cache(dtype=7)) == B.RECO_ERR_UNSUPPORTED
     assert _score(ok, ws=0) == B.RECO_ERR_WORKSPACE
@@ -102,11 +104,12 @@ def test_select_compact_rejects_bad_arguments():
     lib = B.load_library()
     c = _fake_cache()
 
-    def call(cache=c, scores=0x20, ret=0x40, w=8, idx=None, ws=0x30, wsb=1 << 30, layer0=0, nl=2):
-        return lib.reco_select_compact(ctypes.byref(cache), layer0, nl, P(scores), P(ret), w, P(idx) if idx else None,
-                                       P(ws), wsb, None, None)
+    def call(cache=c, scores=0x20, ret=0x40, stride=0, w=8, idx=None, ws=0x30, wsb=1 << 30, layer0=0, nl=2):
+        return lib.reco_select_compact(ctypes.byref(cache), layer0, nl, P(scores), P(ret), stride, w,
+                                       P(idx) if idx else None, P(ws), wsb, None, None)
     assert call(scores=0) == B.RECO_ERR_INVALID_ARG
     assert call(ret=0) == B.RECO_ERR_INVALID_ARG
+    assert call(stride=-1) == B.RECO_ERR_INVALID_ARG
     assert call(w=0) == B.RECO_ERR_INVALID_ARG
     assert call(w=65) == B.RECO_ERR_INVALID_ARG
     assert call(layer0=-1) == B.RECO_ERR_INVALID_ARG
@@ -117,13 +120,44 @@ def test_select_compact_rejects_bad_arguments():
     assert call(wsb=need - 1) == B.RECO_ERR_WORKSPACE
 
 
+def test_pool_scores_rejects_bad_arguments():
+    lib = B.load_library()
+    c = _fake_cache()
+    nbytes = 2 * 1 * 2 * 64 * 4
+
+    def call(cache=c, scores=0x100000, pooled=0x200000, w=8, kernel=5, mode=B.RECO_POOL_MAX, layer0=0, nl=2):
+        return lib.reco_pool_scores(ctypes.byref(cache), layer0, nl, w, P(scores), P(pooled), kernel, mode, None, None)
+    assert call(scores=0) == B.RECO_ERR_INVALID_ARG
+    assert call(pooled=0) == B.RECO_ERR_INVALID_ARG
+    assert call(kernel=4) == B.RECO_ERR_INVALID_ARG                      # even
+    assert call(kernel=0) == B.RECO_ERR_INVALID_ARG
+    assert call(kernel=67) == B.RECO_ERR_INVALID_ARG                     # halo exceeds the LDS stage
+    assert call(mode=2) == B.RECO_ERR_INVALID_ARG
+    assert call(w=0) == B.RECO_ERR_INVALID_ARG
+    assert call(nl=3) == B.RECO_ERR_INVALID_ARG
+    assert call(pooled=0x100000 + nbytes - 4) == B.RECO_ERR_INVALID_ARG  # overlapping buffers
+    assert call(pooled=0x100000 - nbytes + 4) == B.RECO_ERR_INVALID_ARG
+
+
+def test_layer_retention_matches_oracle_exactly():
+    for NL in (1, 2, 28, 32, 64):
+        for r in (0.15, 0.25, 0.5807587504386902, 0.8, 1.0):
+            for rho in (0.0, 0.3, 0.5, 0.9):
+                for l in range(NL):
+                    assert B.reco_layer_retention(r, l, NL, rho) == oracle.layer_retention(r, l, NL, rho)
+    import math
+    for bad in [(0.0, 0, 4, 0.5), (1.5, 0, 4, 0.5), (0.5, 4, 4, 0.5), (0.5, -1, 4, 0.5), (0.5, 0, 4, 1.0),
+                (0.5, 0, 0, 0.5), (0.5, 0, 4, -0.1)]:
+        assert math.isnan(B.reco_layer_retention(*bad)), bad
+
+
 def test_decode_rejects_bad_arguments():
     lib = B.load_library()
     c = _fake_cache()
 
     def call(cache=c, q=0x10, hq=4, scale=0.1, kn=None, vn=None, out=0x50, ws=0x30, wsb=1 << 30):
         return lib.reco_decode_attn(ctypes.byref(cache), 0, 2, P(q), hq, scale, P(kn) if kn else None,
-                                    P(vn) if vn else None, P(out), None, P(ws), wsb, None, None)
+                                    P(vn) if vn else None, P(out), None, None, P(ws), wsb, None, None)
     assert call(q=0) == B.RECO_ERR_INVALID_ARG
     assert call(out=0) == B.RECO_ERR_INVALID_ARG
     assert call(kn=0x60) == B.RECO_ERR_INVALID_ARG                        # k_new without v_new

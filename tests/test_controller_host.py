@@ -65,3 +65,32 @@ def test_steady_state_cache_length():
         assert compress
         s.compressed(r)
     assert abs(s.length - 0.85 * 200 / 0.15) <= 2
+
+
+def test_delta_zero_is_the_uniform_retention_ablation():
+    pol = RecoPolicy(retention="eq1", lam=0.25, delta=0.0, window=32)
+    s = RewardSchedule(pol, prompt_len=512)
+    for v in np.random.default_rng(1).beta(2, 5, size=30):
+        s.token_appended(100)
+        compress, r, _ = s.end_step(float(v))
+        assert compress and r == 0.25
+        s.compressed(r)
+
+
+def test_per_layer_lengths_follow_the_layer_budgets():
+    NL = 6
+    pol = RecoPolicy(retention="clamp", window=16, layer_spread=0.5)
+    s = RewardSchedule(pol, prompt_len=1000, n_layers=NL)
+    ref = [1000] * NL
+    rng = np.random.default_rng(2)
+    for _ in range(12):
+        n = int(rng.integers(10, 300))
+        s.token_appended(n)
+        v = float(rng.uniform())
+        compress, r, _ = s.end_step(v)
+        assert compress and r == oracle.retention_from_reward(v)
+        s.compressed(r)
+        ref = [oracle.kept_count(L + n, 16, oracle.layer_retention(r, l, NL, 0.5)) for l, L in enumerate(ref)]
+        assert s.lengths == ref
+    assert s.lengths[0] > s.lengths[-1]                      # deeper layers keep less
+    assert s.length == s.lengths[0] == s.length_at_compress

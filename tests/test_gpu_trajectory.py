@@ -21,8 +21,17 @@ from paper_2608_04771_amd.controller import RecoDecoder, RecoPolicy
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("retention,dtype", [("clamp", "f32"), ("eq1", "f32"), ("clamp", "bf16")])
-def test_trajectory_matches_oracle_replay(retention, dtype):
+VARIANTS = [
+    ("clamp", "f32", {}), ("eq1", "f32", {}), ("clamp", "bf16", {}),
+    ("eq1", "f32", {"delta": 0.0}),                                   # uniform retention: the paper's ablation
+    ("clamp", "f32", {"layer_spread": 0.5}),                          # per-layer budgets
+    ("eq1", "bf16", {"pool_kernel": 7, "pool_mode": "max"}),          # pooled scores
+    ("clamp", "f32", {"pool_kernel": 5, "pool_mode": "mean", "layer_spread": 0.3}),
+]
+
+
+@pytest.mark.parametrize("retention,dtype,variant", VARIANTS)
+def test_trajectory_matches_oracle_replay(retention, dtype, variant):
     NL, Bsz, H, Hq, D, w = 2, 2, 2, 8, 64, 16
     prompt, n_tokens, cap = 150, 360, 600
     vocab, n_refl = 1000, 16
@@ -52,7 +61,7 @@ def test_trajectory_matches_oracle_replay(retention, dtype):
     rewards[len(bounds) // 2] = 0.9                      # exercise the top band and the probe
     rewards[len(bounds) // 2 + 1] = 0.95
 
-    pol = RecoPolicy(retention=retention, window=w, interval=0)
+    pol = RecoPolicy(retention=retention, window=w, interval=0, **variant)
     cache = B.KVCache(k.to(dev), v.to(dev), ln.to(dev))
     dec = RecoDecoder(cache, Hq, pol, prompt_q.to(dev), torch.from_numpy(refl).to(dev), record_kept=True)
 
@@ -63,7 +72,7 @@ def test_trajectory_matches_oracle_replay(retention, dtype):
     scale = 1 / math.sqrt(D)
     G = Hq // H
     z_dev = logits.to(dev)
-    bi, probes = 0, []
+    bi, probes, fed = 0, [], []
     for tok in range(n_tokens):
         out, lse = dec.decode(qs[tok].to(dev), ks[tok].to(dev), vs[tok].to(dev), logits=z_dev[tok])
         ref, rl = oracle.decode_cache(K, V, lens, f64(qs[tok]), scale, f64(ks[tok]), f64(vs[tok]))
@@ -76,28 +85,34 @@ def test_trajectory_matches_oracle_replay(retention, dtype):
             vb = rewards[bi]
             compressed, probe = dec.end_step(vb)
             probes.append(probe)
+            fed.append(dec.last_score_stats_fed)
             assert compressed
             r = []
             for b in range(Bsz):
                 hist[b].append(float(vb[b]))
-                r.append(oracle.retention_eq1(hist[b], 0.25, 0.1) if retention == "eq1"
+                r.append(oracle.retention_eq1(hist[b], 0.25, pol.delta) if retention == "eq1"
                          else oracle.retention_from_reward(vb[b]))
             s_or = oracle.score_cache(K, lens, win, scale)
             torch.cuda.synchronize()
             kept = dec.kept.cpu().numpy()
             for u in np.ndindex(NL, Bsz, H):
                 L = int(lens[u])
-                ok, msg = kept_sets_match(kept[u], s_or[u], L, w, r[u[1]])
+                r_u = oracle.layer_retention(r[u[1]], u[0], NL, pol.layer_spread)
+                s_u = s_or[u]
+                if pol.pool_kernel > 1:
+                    s_u = oracle.pool_scores(s_u, L, w, pol.pool_kernel, pol.pool_mode)
+                ok, msg = kept_sets_match(kept[u], s_u, L, w, r_u)
                 assert ok, (tok, u, msg)
-                m = oracle.kept_count(L, w, r[u[1]])
+                m = oracle.kept_count(L, w, r_u)
                 idx = kept[u][:m]
                 K[u][:m], V[u][:m] = K[u][idx].copy(), V[u][idx].copy()
                 lens[u] = m
             assert (dec.cache.length.cpu().numpy() == lens).all()
-            assert dec.lengths() == [int(lens[0, b, 0]) for b in range(Bsz)]
+            assert dec.layer_lengths() == [[int(lens[l, b, 0]) for l in range(NL)] for b in range(Bsz)]
             band = np.asarray(vb, dtype=np.float32)
             bi += 1
     assert dec.dev_err.item() == 0
+    assert any(fed) and not all(fed)          # both the one-pass (decode statistics) and two-pass scoring ran
     expect = [[i > 0 and rewards[i][b] >= 0.8 and rewards[i - 1][b] >= 0.8 for b in range(Bsz)]
               for i in range(len(bounds))]
     assert probes == expect

@@ -48,9 +48,9 @@ ANSWER_LEN = 32
 DECODE_TRAFFIC = {
     "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
                 "paper_2608_04771_amd/csrc/decode_attn.hpp"),
-    "sha256": "2fb656c3a02644e4766d747b5b48ae6291724ac2158bbcd15e50f4173dfb8ef5",
+    "sha256": "1f0db65235b36d3aab8e6f93eb672001ff79024ce4b82e6554d95914f7058f19",
     "workload": "7b-28L-28q4kv-d128-bf16-L16384",
-    "fetch_bytes": 555323104,
+    "fetch_bytes": 555382986,
     "write_bytes": 817152,
 }
 
@@ -111,6 +111,8 @@ class Workload:
         self.ws_smp = torch.empty(B.penalty_sample_workspace_size(wl.decode_steps * Bsz, V), dtype=torch.uint8,
                                   device=dev)
         self.tokens = torch.empty(wl.decode_steps * Bsz, dtype=torch.int32, device=dev)
+        # (max, sum) softmax statistics of every decode query, kept for one-pass scoring
+        self.stats = torch.empty((wl.decode_steps, NL, Bsz, wl.n_q_heads, 2), dtype=torch.float32, device=dev)
         self.out = torch.empty_like(self.q[0])
         self.lse = torch.empty(self.q.shape[1:4], dtype=torch.float32, device=dev)
         self.ppl = torch.empty(Bsz, dtype=torch.float32, device=dev)
@@ -143,7 +145,7 @@ class Workload:
                                   dev_err=self.dev_err)
         for s in range(wl.decode_steps):
             B.reco_decode_attn(cache, self.q[s], self.k_new[s], self.v_new[s], out=self.out, lse=self.lse,
-                               ws=self.ws_dec, dev_err=self.dev_err)
+                               ws=self.ws_dec, dev_err=self.dev_err, row_stats=self.stats[s])
         if ev is not None:
             ev["d1"].record()
         main.wait_stream(self.side)
@@ -153,6 +155,34 @@ class Workload:
                           dev_err=self.dev_err)
         if ev is not None:
             ev["p1"].record()
+
+
+def score_after_decode(w: Workload, i: int, reps: int = 5):
+    """Scoring of the post-decode cache of copy i with its last `window`
+    decode tokens as the window, once with the two-pass kernels and once fed
+    with the statistics those decode calls wrote (no compression happened
+    since, so both compute Eq. 2 over the same keys).  Outside the timed step."""
+    wl = w.wl
+    win = wl.window
+    cache = B.KVCache(*w.copies[i])
+    q_win = w.q[-win:].permute(1, 2, 3, 0, 4).contiguous()          # [NL][B][Hq][w][D]
+    st_win = w.stats[-win:].permute(1, 2, 3, 0, 4).contiguous()      # [NL][B][Hq][w][2]
+    a, b = torch.zeros_like(w.scores), torch.zeros_like(w.scores)
+    E = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    out = {}
+    for name, stats, dst in (("two_pass", None, a), ("stats_fed", st_win, b)):
+        B.reco_score(cache, q_win, win, scores=dst, ws=w.ws_score, dev_err=w.dev_err, row_stats=stats)
+        e0, e1 = E(), E()
+        e0.record()
+        for _ in range(reps):
+            B.reco_score(cache, q_win, win, scores=dst, ws=w.ws_score, dev_err=w.dev_err, row_stats=stats)
+        e1.record()
+        torch.cuda.synchronize()
+        out[name + "_ms"] = e0.elapsed_time(e1) / reps
+    rel = ((b - a).abs() / a.clamp_min(1e-30)).masked_fill(a <= 1e-20, 0.0)
+    out["max_rel_diff"] = float(rel.max().item())
+    out["cache_rows"] = int(cache.length.max().item())
+    return out
 
 
 def make_events():
@@ -278,6 +308,7 @@ def main():
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
+    score_fed = score_after_decode(w, args.warmup + args.steps - 1)
 
     # Sizes of this workload's steps (identical for every copy).
     lens_after = w.copies[args.warmup][2].cpu().numpy()
@@ -329,6 +360,7 @@ def main():
         "phase_ms": {"score": float(score_ms.mean()), "select_compact": float(sel_ms.mean()),
                      "compress": float(comp_ms.mean()), "decode_call": dec_avg_ms,
                      "decode_calls_total": float(dec_loop_ms.mean()), "answer_ppl": float(ppl_ms.mean())},
+        "score_after_decode": score_fed,
         "roofline": {"kernel": "reco_decode_attn (decode_split_kernel + decode_merge_kernel)", "bound": "hbm",
                      "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
                      "traffic": decode_traffic(wl.name), "traffic_unit": "bytes per decode_split_kernel launch",

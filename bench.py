@@ -48,9 +48,9 @@ ANSWER_LEN = 32
 DECODE_TRAFFIC = {
     "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
                 "paper_2608_04771_amd/csrc/decode_attn.hpp"),
-    "sha256": "1f0db65235b36d3aab8e6f93eb672001ff79024ce4b82e6554d95914f7058f19",
+    "sha256": "c4ae390db1acee3947a7e6d0547b201ad82edf9d7ec2035c25ff28b7dba79ab1",
     "workload": "7b-28L-28q4kv-d128-bf16-L16384",
-    "fetch_bytes": 555382986,
+    "fetch_bytes": 555283181,
     "write_bytes": 817152,
 }
 

@@ -96,25 +96,37 @@ __device__ __forceinline__ T lds_elem(const unsigned char *p) {
   return *reinterpret_cast<const T *>(p);
 }
 
-// Gather the V^T fragment of MFMA `c` for head-dim column `dcol` from the
-// staged tile: element j holds key (e / 4) * 16 + 4 * grp + (e % 4), e = c * kpl + j.
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+
+// Gather the V^T fragment of MFMA `c` for head-dim tile `dt` from the staged
+// tile: lane (col, grp) needs, at head-dim column dt*16 + col, the keys of
+// element e = c * kpl + j, key (e / 4) * 16 + 4 * grp + (e % 4).
+// bf16: two LDS transpose reads.  Within each 16-lane group, lane j supplies
+// the 8 bytes at row key0 + j / 4, columns d0 + 4 * (j % 4) .. + 3, and lane i
+// receives element i % 4 of the rows supplied by lanes 4r + i / 4, r = 0..3,
+// i.e. column d0 + i of rows key0 .. key0 + 3: four consecutive keys of one
+// head-dim column, as the operand wants.
 template <typename T, int D>
-__device__ __forceinline__ typename Mfma<T>::frag vt_frag(const unsigned char *stage, int c, int grp,
-                                                          int dcol) {
+__device__ __forceinline__ typename Mfma<T>::frag vt_frag(const unsigned char *stage, int c, int grp, int dt,
+                                                          int col) {
   using Cfg = DecodeCfg<T, D>;
   typename Mfma<T>::frag a;
   if constexpr (Cfg::kpl == 1) {
     const int e = c;
     const int kl = (e >> 2) * 16 + 4 * grp + (e & 3);
-    a = lds_elem<float>(stage + kl * Cfg::lds_stride + dcol * 4);
+    a = lds_elem<float>(stage + kl * Cfg::lds_stride + (dt * 16 + col) * 4);
   } else {
+    static_assert(Cfg::lds_stride % 8 == 0, "transpose reads need 8-byte aligned rows");
+    const int key0 = 32 * c + 4 * grp + col / 4;
+    const int cb = (dt * 16 + 4 * (col % 4)) * 2;
+    const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4_t *)(stage + key0 * Cfg::lds_stride + cb));
+    const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4_t *)(stage + (key0 + 16) * Cfg::lds_stride + cb));
+    const short v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 #pragma unroll
-    for (int j = 0; j < Cfg::kpl; ++j) {
-      const int e = c * Cfg::kpl + j;
-      const int kl = (e >> 2) * 16 + 4 * grp + (e & 3);
-      const uint16_t bits = *reinterpret_cast<const uint16_t *>(stage + kl * Cfg::lds_stride + dcol * 2);
-      a[j] = __builtin_bit_cast(__bf16, bits);
-    }
+    for (int j = 0; j < 8; ++j) a[j] = __builtin_bit_cast(__bf16, v[j]);
   }
   return a;
 }
@@ -259,7 +271,7 @@ __global__ __launch_bounds__(kThreads, (DecodeCfg<T, D>::min_wgs)) void decode_s
     for (int dt = 0; dt < Cfg::dtiles; ++dt) {
 #pragma unroll
       for (int c = 0; c < Cfg::pv_ops; ++c) {
-        const frag a = vt_frag<T, D>(stage, c, grp, dt * 16 + col);
+        const frag a = vt_frag<T, D>(stage, c, grp, dt, col);
         o[dt] = MF::mma(a, pt_frag<T>(pv, c), o[dt]);
       }
     }

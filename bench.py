@@ -140,9 +140,13 @@ class Workload:
             ev["c2"].record()
         self.side.wait_stream(main)
         with torch.cuda.stream(self.side):
+            if ev is not None:
+                ev["s0"].record()
             B.reco_penalty_sample(self.logits.view(-1, self.logits.shape[-1]), self.refl, self.row_reward, TAU_LO,
                                   TAU_HI, *BETAS, TEMPERATURE, SAMPLE_SEED, i, tokens=self.tokens, ws=self.ws_smp,
                                   dev_err=self.dev_err)
+            if ev is not None:
+                ev["s1"].record()
         for s in range(wl.decode_steps):
             B.reco_decode_attn(cache, self.q[s], self.k_new[s], self.v_new[s], out=self.out, lse=self.lse,
                                ws=self.ws_dec, dev_err=self.dev_err, row_stats=self.stats[s])
@@ -185,9 +189,64 @@ def score_after_decode(w: Workload, i: int, reps: int = 5):
     return out
 
 
+def decode_per_layer_graph(w: Workload, i: int, reps: int = 20):
+    """The model-faithful form of one decode step: one reco_decode_attn call
+    per layer (as a model interleaves them with its other layers), the
+    NL calls captured once in a HIP graph and replayed.  Runs on the
+    post-decode cache of copy i (each replay appends one more token),
+    outside the timed step."""
+    wl = w.wl
+    NL = w.shape[0]
+    cache = B.KVCache(*w.copies[i])
+    q, kn, vn = w.q[0], w.k_new[0], w.v_new[0]
+    ws = torch.empty(B.decode_attn_workspace_size(cache, wl.n_q_heads, 1), dtype=torch.uint8, device=q.device)
+    out = torch.empty_like(q)
+    lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+
+    def one_step():
+        for l in range(NL):
+            B.reco_decode_attn(cache, q[l:l + 1], kn[l:l + 1], vn[l:l + 1], out=out[l:l + 1], lse=lse[l:l + 1],
+                               layer0=l, n_layers=1, ws=ws, dev_err=w.dev_err)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        one_step()                                     # warm-up outside the capture
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        one_step()
+    g.replay()
+    torch.cuda.synchronize()
+    E = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    e0, e1 = E(), E()
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return {"us_per_decode_step": e0.elapsed_time(e1) * 1e3 / reps, "calls_per_step": NL,
+            "cache_rows": int(cache.length.max().item())}
+
+
+def copy_bandwidth(w: Workload):
+    """Context: a plain device-to-device copy of one cache's K (read + write)."""
+    src = w.copies[0][0]
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    E = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    e0, e1 = E(), E()
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    return 2 * src.numel() * src.element_size() * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+
+
 def make_events():
     E = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
-    return {"c0": E(), "c1": E(), "c2": E(), "d1": E(), "p0": E(), "p1": E()}
+    return {"c0": E(), "c1": E(), "c2": E(), "d1": E(), "p0": E(), "p1": E(), "s0": E(), "s1": E()}
 
 
 def algorithmic_bytes(w: Workload, m: np.ndarray, moved_rows: int):
@@ -309,6 +368,8 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
     score_fed = score_after_decode(w, args.warmup + args.steps - 1)
+    per_layer = decode_per_layer_graph(w, args.warmup + args.steps - 1)
+    copy_gbps = copy_bandwidth(w)
 
     # Sizes of this workload's steps (identical for every copy).
     lens_after = w.copies[args.warmup][2].cpu().numpy()
@@ -331,6 +392,7 @@ def main():
     score_ms = np.array([ev["c0"].elapsed_time(ev["c1"]) for ev in evs])
     sel_ms = np.array([ev["c1"].elapsed_time(ev["c2"]) for ev in evs])
     ppl_ms = np.array([ev["p0"].elapsed_time(ev["p1"]) for ev in evs])
+    smp_ms = np.array([ev["s0"].elapsed_time(ev["s1"]) for ev in evs])
     dec_bytes_mean = float(np.mean(ab["decode"]))
     dec_avg_ms = float(dec_loop_ms.mean()) / wl.decode_steps
     achieved = dec_bytes_mean / (dec_avg_ms * 1e-3) / 1e9
@@ -361,6 +423,11 @@ def main():
                      "compress": float(comp_ms.mean()), "decode_call": dec_avg_ms,
                      "decode_calls_total": float(dec_loop_ms.mean()), "answer_ppl": float(ppl_ms.mean())},
         "score_after_decode": score_fed,
+        "decode_per_layer_graph": per_layer,
+        "penalty_sample": {"ms_per_step": float(smp_ms.mean()), "rows_per_step": int(w.tokens.numel()),
+                           "us_per_row": float(smp_ms.mean()) * 1e3 / int(w.tokens.numel()),
+                           "stream": "side (overlaps the decode calls)"},
+        "copy_GBps_context": copy_gbps,
         "roofline": {"kernel": "reco_decode_attn (decode_split_kernel + decode_merge_kernel)", "bound": "hbm",
                      "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
                      "traffic": decode_traffic(wl.name), "traffic_unit": "bytes per decode_split_kernel launch",

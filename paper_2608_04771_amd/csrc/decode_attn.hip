@@ -423,13 +423,131 @@ __global__ __launch_bounds__(kWave) void decode_merge_kernel(DecodeParams p) {
   if (lane == 0) p.len[cunit] = len_in + 1;
 }
 
+// Merge for many splits (small calls, e.g. one layer per call): one
+// 256-thread workgroup per (unit, query head).  Every split's output slice is
+// requested at once (thread group sg loads splits sg, sg + kSG, ... as 16-byte
+// pieces) together with the split statistics, so the merge costs one memory
+// round trip whatever the split count; the weighted slices meet in LDS.
+constexpr int kWideThreads = 256;
+constexpr int kWideMinSplits = 9;                  // fewer splits use the one-wave merge
+
+template <typename T, int D>
+__global__ __launch_bounds__(kWideThreads) void decode_merge_wide_kernel(DecodeParams p) {
+  constexpr int kVec = 4;
+  constexpr int kTPS = D / kVec;                   // threads per split slice
+  constexpr int kSG = kWideThreads / kTPS;         // split groups
+  constexpr int kMaxPer = kMaxSplits / kSG;        // splits per thread at most
+  constexpr int kWaves = kWideThreads / kWave;
+  __shared__ float s_w[kMaxSplits];
+  __shared__ float s_red[kWaves];
+  __shared__ __attribute__((aligned(16))) float s_acc[kSG][D];
+
+  const int unit = blockIdx.x;
+  const int qi = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  const int per_layer = p.batch * p.hkv;
+  const int lc = unit / per_layer;
+  const int b = (unit % per_layer) / p.hkv;
+  const int h = unit % p.hkv;
+  const size_t cunit = (static_cast<size_t>(p.layer0 + lc) * p.batch + b) * p.hkv + h;
+  const size_t qunit = static_cast<size_t>(lc) * per_layer + static_cast<size_t>(b) * p.hkv + h;
+  const int S = p.splits;
+  const bool append = p.k_new != nullptr && qi == 0;
+
+  // Everything this workgroup reads is requested up front.
+  const int len_in = qi == 0 ? p.len[cunit] : 0;
+  T krow = T{}, vrow = T{};
+  if (append && tid < D) {
+    krow = reinterpret_cast<const T *>(p.k_new)[qunit * D + tid];
+    vrow = reinterpret_cast<const T *>(p.v_new)[qunit * D + tid];
+  }
+  const int sg = tid / kTPS;
+  const int dv = (tid % kTPS) * kVec;
+  const float *po = p.part_o + (static_cast<size_t>(unit) * S * 16 + qi) * D;
+  float4 part[kMaxPer];
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    const int sp = sg + kSG * i;
+    part[i] = sp < S ? *reinterpret_cast<const float4 *>(po + static_cast<size_t>(sp) * 16 * D + dv)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  const float *pml = p.part_ml + static_cast<size_t>(unit) * S * 32;
+  const float m_t = tid < S ? pml[tid * 32 + qi] : -INFINITY;
+  const float l_t = tid < S ? pml[tid * 32 + 16 + qi] : 0.f;
+
+  // M = max of the split maxima, L = sum of the rescaled split sums.
+  float v = wave_max(m_t);
+  if (lane == 0) s_red[wave] = v;
+  __syncthreads();
+  float M = s_red[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) M = fmaxf(M, s_red[w]);
+  __syncthreads();
+  const float e_t = (M != -INFINITY && tid < S) ? fast_exp2(m_t - M) : 0.f;
+  v = wave_sum(l_t * e_t);
+  if (lane == 0) s_red[wave] = v;
+  __syncthreads();
+  float L = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) L += s_red[w];
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  if (tid < kMaxSplits) s_w[tid] = e_t * inv;
+  __syncthreads();
+
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    const int sp = sg + kSG * i;
+    const float wgt = sp < S ? s_w[sp] : 0.f;
+    acc.x += wgt * part[i].x;
+    acc.y += wgt * part[i].y;
+    acc.z += wgt * part[i].z;
+    acc.w += wgt * part[i].w;
+  }
+  *reinterpret_cast<float4 *>(&s_acc[sg][dv]) = acc;
+  __syncthreads();
+
+  const size_t oq = (static_cast<size_t>(lc) * p.batch + b) * p.hq + h * p.group + qi;
+  if (tid < D) {
+    float o = 0.f;
+#pragma unroll
+    for (int g = 0; g < kSG; ++g) o += s_acc[g][tid];
+    reinterpret_cast<T *>(p.out)[oq * D + tid] = from_f32<T>(o);
+  }
+  if (tid == 0) {
+    if (p.lse) p.lse[oq] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+    if (p.row_stats) {
+      p.row_stats[oq * 2 + 0] = M;
+      p.row_stats[oq * 2 + 1] = L;
+    }
+  }
+
+  if (qi != 0) return;
+  if (tid == 0 && (len_in < 0 || len_in > p.cap)) report(p.dev_err, 5 /*RECO_DEV_BAD_LENGTH*/);
+  if (!append || len_in < 0 || len_in > p.cap) return;
+  if (len_in == p.cap) {
+    if (tid == 0) report(p.dev_err, 1 /*RECO_DEV_APPEND_OVERFLOW*/);
+    return;
+  }
+  if (tid < D) {
+    reinterpret_cast<T *>(p.k)[(cunit * p.cap + len_in) * D + tid] = krow;
+    reinterpret_cast<T *>(p.v)[(cunit * p.cap + len_in) * D + tid] = vrow;
+  }
+  if (tid == 0) p.len[cunit] = len_in + 1;
+}
+
 template <typename T, int D>
 hipError_t launch_typed(const DecodeParams &p, hipStream_t s) {
   const int units = p.n_layers * p.batch * p.hkv;
   hipLaunchKernelGGL((decode_split_kernel<T, D>), dim3(p.splits, units), dim3(kThreads), 0, s, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((decode_merge_kernel<T, D>), dim3(units, p.group), dim3(kWave), 0, s, p);
+  if (p.splits >= kWideMinSplits)
+    hipLaunchKernelGGL((decode_merge_wide_kernel<T, D>), dim3(units, p.group), dim3(kWideThreads), 0, s, p);
+  else
+    hipLaunchKernelGGL((decode_merge_kernel<T, D>), dim3(units, p.group), dim3(kWave), 0, s, p);
   return hipGetLastError();
 }
 

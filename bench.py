@@ -10,7 +10,7 @@ One step = one pass of the whole path over one batch of synthetic input:
 Every step starts from its own pristine copy of the cache, staged in HBM
 before the timed region.  Prints one JSON line (rank 0, N = 1).
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 7b16k]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 7b16k] [--no-cpu-baseline] [--no-extras]
 """
 from __future__ import annotations
 
@@ -48,9 +48,9 @@ ANSWER_LEN = 32
 DECODE_TRAFFIC = {
     "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
                 "paper_2608_04771_amd/csrc/decode_attn.hpp"),
-    "sha256": "c4ae390db1acee3947a7e6d0547b201ad82edf9d7ec2035c25ff28b7dba79ab1",
+    "sha256": "ad6cd231e4683449ce16efca9617e3b5daa91dccba60db5b9279b954607e60f0",
     "workload": "7b-28L-28q4kv-d128-bf16-L16384",
-    "fetch_bytes": 555283181,
+    "fetch_bytes": 555130435,
     "write_bytes": 817152,
 }
 
@@ -336,6 +336,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="7b16k", choices=sorted(I.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    ap.add_argument("--no-extras", dest="extras", action="store_false",
+                    help="skip the measurements made after the timed steps (for profiler runs)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -367,9 +369,11 @@ def main():
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
-    score_fed = score_after_decode(w, args.warmup + args.steps - 1)
-    per_layer = decode_per_layer_graph(w, args.warmup + args.steps - 1)
-    copy_gbps = copy_bandwidth(w)
+    score_fed = per_layer = copy_gbps = None
+    if args.extras:
+        score_fed = score_after_decode(w, args.warmup + args.steps - 1)
+        per_layer = decode_per_layer_graph(w, args.warmup + args.steps - 1)
+        copy_gbps = copy_bandwidth(w)
 
     # Sizes of this workload's steps (identical for every copy).
     lens_after = w.copies[args.warmup][2].cpu().numpy()

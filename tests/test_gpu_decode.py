@@ -1,4 +1,6 @@
 """GPU parity of reco_decode_attn against the CPU oracle (decode_cache)."""
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -106,3 +108,30 @@ def test_decode_tiny_workload_64_steps():
         assert_decode_close(out, ref, "f32", f"step {s}")
         assert_lse_close(lse, rl, "f32", f"step {s}")
     assert (cache.length.cpu().numpy() == lens).all()
+
+
+@pytest.mark.parametrize("dtype,D,G", [("bf16", 128, 7), ("f32", 64, 4)])
+def test_decode_single_unit_max_splits(dtype, D, G):
+    """One long unit: the call splits it the maximum 128 ways and merges the
+    splits with the many-split merge; appended row and length checked too."""
+    NL, Bsz, H, Cap = 1, 1, 1, 20000
+    lens = [17001]
+    k, v, ln = _random_cache(NL, Bsz, H, Cap, D, dtype, lens, seed=77)
+    td = k.dtype
+    gq = torch.Generator().manual_seed(6)
+    q = torch.randn((NL, Bsz, H * G, D), generator=gq).to(td)
+    kn = torch.randn((NL, Bsz, H, D), generator=gq).to(td)
+    vn = torch.randn((NL, Bsz, H, D), generator=gq).to(td)
+    cache = B.KVCache(k.cuda(), v.cuda(), ln.cuda())
+    assert B.decode_attn_workspace_size(cache, H * G) >= 128 * (16 * D + 32) * 4
+    dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out, lse = B.reco_decode_attn(cache, q.cuda(), kn.cuda(), vn.cuda(), dev_err=dev_err)
+    torch.cuda.synchronize()
+    assert dev_err.item() == 0
+    n = lens[0]
+    ref, rl = oracle.decode_unit(f64(k[0, 0, 0][:n]), f64(v[0, 0, 0][:n]), n, f64(q[0, 0]), 1 / math.sqrt(D),
+                                 f64(kn[0, 0, 0]), f64(vn[0, 0, 0]))
+    assert_decode_close(out[0, 0], ref, dtype, "single unit")
+    assert_lse_close(lse[0, 0], rl, dtype, "single unit")
+    assert int(cache.length[0, 0, 0].item()) == n + 1
+    assert torch.equal(cache.k[0, 0, 0, n].cpu(), kn[0, 0, 0]) and torch.equal(cache.v[0, 0, 0, n].cpu(), vn[0, 0, 0])

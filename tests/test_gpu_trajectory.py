@@ -86,6 +86,16 @@ def test_trajectory_matches_oracle_replay(retention, dtype, variant):
             compressed, probe = dec.end_step(vb)
             probes.append(probe)
             fed.append(dec.last_score_stats_fed)
+            if any(probe):
+                # Answer probe (Eq. 5-6) on a synthetic 8-token answer; one
+                # sequence's answer is made confident so both stop branches run.
+                ans = torch.randn((Bsz, 8, vocab), generator=g) * 3
+                ans_tok = torch.randint(0, vocab, (Bsz, 8), generator=g, dtype=torch.int32)
+                ans[0, torch.arange(8), ans_tok[0].long()] += 25.0
+                ppl, stop = dec.answer_ppl(ans.to(dev), ans_tok.to(dev))
+                ppl_or, stop_or = oracle.answer_ppl(ans.numpy(), ans_tok.numpy(), pol.tau_p)
+                np.testing.assert_allclose(ppl.cpu().numpy(), ppl_or, rtol=1e-5)
+                assert (stop.cpu().numpy() == stop_or).all() and stop_or[0] and not stop_or[1]
             assert compressed
             r = []
             for b in range(Bsz):
@@ -116,4 +126,5 @@ def test_trajectory_matches_oracle_replay(retention, dtype, variant):
     expect = [[i > 0 and rewards[i][b] >= 0.8 and rewards[i - 1][b] >= 0.8 for b in range(Bsz)]
               for i in range(len(bounds))]
     assert probes == expect
+    assert any(any(p) for p in probes)
     assert all(probes[len(bounds) // 2 + 1])

@@ -197,8 +197,11 @@ constexpr int kPplThreads = 256;
 constexpr int kPplChunk = 16384;   // logits per workgroup
 
 // Per (row, chunk): the chunk's max and sum of exp(z - max), natural log domain.
+// Each thread holds its 64 logits of the chunk in registers (all requested in
+// one round trip), so the max and the sum need a single read of the chunk.
 __global__ __launch_bounds__(kPplThreads) void ppl_partial_kernel(const float *logits, int vocab, int chunks,
                                                                   float *part) {
+  constexpr int kPer = kPplChunk / kPplThreads;
   __shared__ float red[kPplThreads / kWave];
   const int chunk = blockIdx.x;
   const size_t row = blockIdx.y;
@@ -208,8 +211,15 @@ __global__ __launch_bounds__(kPplThreads) void ppl_partial_kernel(const float *l
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
 
+  float x[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int j = c0 + i * kPplThreads + static_cast<int>(threadIdx.x);
+    x[i] = j < c1 ? z[j] : -INFINITY;
+  }
   float m = -INFINITY;
-  for (int j = c0 + threadIdx.x; j < c1; j += kPplThreads) m = fmaxf(m, z[j]);
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) m = fmaxf(m, x[i]);
   m = wave_max(m);
   if (lane == 0) red[wave] = m;
   __syncthreads();
@@ -218,8 +228,10 @@ __global__ __launch_bounds__(kPplThreads) void ppl_partial_kernel(const float *l
   for (int w = 1; w < kPplThreads / kWave; ++w) M = fmaxf(M, red[w]);
   __syncthreads();
   float s = 0.f;
-  if (M != -INFINITY)
-    for (int j = c0 + threadIdx.x; j < c1; j += kPplThreads) s += expf(z[j] - M);
+  if (M != -INFINITY) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) s += expf(x[i] - M);     // x = -inf (past the row) adds 0
+  }
   s = wave_sum(s);
   if (lane == 0) red[wave] = s;
   __syncthreads();

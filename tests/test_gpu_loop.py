@@ -91,8 +91,10 @@ def test_7b16k_full_size_sampled():
     qs, ks, vs = I.make_decode_inputs(wl, ci, steps)
     check_steps = {0, steps // 2, steps - 1}
     ws = B.decode_workspace(cache, wl.n_q_heads)
+    w = wl.window
+    stats = torch.empty((steps, wl.n_layers, 1, wl.n_q_heads, 2), dtype=torch.float32, device="cuda")
     for s in range(steps):
-        out, lse = B.reco_decode_attn(cache, qs[s].cuda(), ks[s].cuda(), vs[s].cuda(), ws=ws)
+        out, lse = B.reco_decode_attn(cache, qs[s].cuda(), ks[s].cuda(), vs[s].cuda(), ws=ws, row_stats=stats[s])
         if s in check_steps:
             torch.cuda.synchronize()
             assert torch.isfinite(out.float()).all()
@@ -104,3 +106,18 @@ def test_7b16k_full_size_sampled():
                 assert_decode_close(out[l, b, h * G:(h + 1) * G], ref, "bf16", f"step {s} unit {(l, b, h)}")
                 assert_lse_close(lse[l, b, h * G:(h + 1) * G], rl, "bf16", f"step {s} unit {(l, b, h)}")
     assert (cache.length.cpu().numpy() == m + steps).all()
+    # One-pass scoring of the post-decode cache, fed with the decode statistics
+    # of the last w tokens (no compression since), against the two-pass kernels
+    # and the oracle on the sampled units.
+    q_win = torch.stack([q.cuda() for q in qs[-w:]], dim=3).contiguous()        # [NL][B][Hq][w][D]
+    st_win = stats[-w:].permute(1, 2, 3, 0, 4).contiguous()
+    s_fed = B.reco_score(cache, q_win, w, row_stats=st_win).cpu().numpy().astype(np.float64)
+    s_two = B.reco_score(cache, q_win, w).cpu().numpy().astype(np.float64)
+    n = m + steps
+    big = s_two[..., :n] > 1e-20
+    assert (np.abs(s_fed[..., :n] - s_two[..., :n])[big] / s_two[..., :n][big]).max() <= SCORE_RTOL
+    for (l, b, h) in units:
+        s_or = oracle.score_unit(f64(cache.k[l, b, h, :n]), f64(q_win[l, b, h * G:(h + 1) * G]), scale)
+        assert (np.abs(s_fed[l, b, h, :n] - s_or) / s_or).max() <= SCORE_RTOL
+        ok, msg = kept_sets_match(oracle.select_unit(s_fed[l, b, h], n, w, 0.5), s_or, n, w, 0.5)
+        assert ok, msg

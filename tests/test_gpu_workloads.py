@@ -31,11 +31,17 @@ def _run_workload(wl, units, decode_steps, check_steps, seq_lens=None):
     before = {u: (f64(ci.k[u][:int(lens0[u])]), f64(ci.v[u][:int(lens0[u])])) for u in units}
     qwin = {u: f64(ci.q_win[u[0], u[1], u[2] * G:(u[2] + 1) * G]) for u in units}
 
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ev[0].record()
     scores = B.reco_score(cache, ci.q_win, wl.window)
     kept = torch.full((NL, Bsz, H, Cap), -1, dtype=torch.int32, device=dev)
     dev_err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ev[1].record()
     B.reco_select_compact(cache, scores, torch.from_numpy(r).to(dev), wl.window, kept_idx=kept, dev_err=dev_err)
+    ev[2].record()
     torch.cuda.synchronize()
+    print(f"{wl.name}: score {ev[0].elapsed_time(ev[1]):.2f} ms, select+compact {ev[1].elapsed_time(ev[2]):.2f} ms "
+          f"over {int(lens0.sum())} cached rows")
     assert dev_err.item() == 0
     m_all = np.array([[oracle.kept_count(int(lens0[0, b, 0]), wl.window, r[b]) for b in range(Bsz)]])
     lens1 = cache.length.cpu().numpy()
@@ -71,6 +77,18 @@ def _run_workload(wl, units, decode_steps, check_steps, seq_lens=None):
     torch.cuda.synchronize()
     assert dev_err.item() == 0
     assert (cache.length.cpu().numpy() == lens1 + decode_steps).all()
+    # Timing of back-to-back decode calls (all layers per call) after the checks.
+    n_rows = int(cache.length.sum().item())
+    ws = B.decode_workspace(cache, wl.n_q_heads)
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for s in range(2):
+        B.reco_decode_attn(cache, qs[s], ks[s], vs[s], ws=ws)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / 2
+    gb = (n_rows + 1.5 * cache.length.numel()) * 2 * D * 2 / 1e9
+    print(f"{wl.name}: decode call {ms:.2f} ms for {gb:.1f} GB of K/V -> {gb / ms:.2f} TB/s")
     return ci, cache
 
 

@@ -244,8 +244,7 @@ __global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreParams p) {
 template <typename T, int D, int RTW, bool FULL>
 __device__ __forceinline__ void mass_block(const ScoreParams &p, const UnitInfo &u, const RowBlock<T, D, RTW> &rb,
                                            const unsigned char *stage, int kb, int tile0, int col, int grp,
-                                           const float (&rmax)[RTW][4], const float (&rinv)[RTW][4],
-                                           float (&acc)[2]) {
+                                           const float *smax, const float *sinv, float (&acc)[2]) {
   using MF = Mfma<T>;
   using Cfg = ScoreCfg<T, D>;
 #pragma unroll
@@ -258,17 +257,21 @@ __device__ __forceinline__ void mass_block(const ScoreParams &p, const UnitInfo 
       f32x4_t s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int c = 0; c < Cfg::steps; ++c) s = MF::mma(rb.q[k][c], kf[c], s);
+      const float4 mx = *reinterpret_cast<const float4 *>(smax + k * 16 + 4 * grp);
+      const float4 iv = *reinterpret_cast<const float4 *>(sinv + k * 16 + 4 * grp);
+      const float rmax[4] = {mx.x, mx.y, mx.z, mx.w};
+      const float rinv[4] = {iv.x, iv.y, iv.z, iv.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         // Absent rows carry max = +inf and 1/sum = 0, so they add exactly 0.
-        const float e = fast_exp2(fmaf(s[i], p.scale_log2, -rmax[k][i]));
+        const float e = fast_exp2(fmaf(s[i], p.scale_log2, -rmax[i]));
         if constexpr (FULL) {
-          acc[kt] = fmaf(e, rinv[k][i], acc[kt]);
+          acc[kt] = fmaf(e, rinv[i], acc[kt]);
         } else {
           const int r = (tile0 + k) * 16 + 4 * grp + i;
           const int pos = u.L - p.w + r % p.w;
           const bool vis = key < u.L && (!p.causal || key <= pos);
-          acc[kt] += vis ? e * rinv[k][i] : 0.f;
+          acc[kt] += vis ? e * rinv[i] : 0.f;
         }
       }
     }
@@ -276,12 +279,17 @@ __device__ __forceinline__ void mass_block(const ScoreParams &p, const UnitInfo 
 }
 
 template <typename T, int D, int RTW>
-__global__ __launch_bounds__(kThreads) void score_mass_kernel(ScoreParams p) {
+// Two workgroups per CU (two waves per SIMD): the window rows' normalisers sit
+// in LDS rather than registers, which (with a small spill) fits 256 registers
+// and measured faster than one wave per SIMD with everything in registers.
+__global__ __launch_bounds__(kThreads, 2) void score_mass_kernel(ScoreParams p) {
   constexpr int n_waves = kWaves;
   using Cfg = ScoreCfg<T, D>;
   using RB = RowBlock<T, D, RTW>;
   __shared__ __attribute__((aligned(16))) unsigned char stage[2][Cfg::stage_bytes];
   __shared__ float part[kWaves][kScoreChunk];
+  __shared__ __attribute__((aligned(16))) float s_max[kWaves * RTW * 16];
+  __shared__ __attribute__((aligned(16))) float s_inv[kWaves * RTW * 16];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int col = lane & 15, grp = lane >> 4;
@@ -300,19 +308,16 @@ __global__ __launch_bounds__(kThreads) void score_mass_kernel(ScoreParams p) {
     const int tile0 = tg + wave * RTW;
     RB rb;
     rb.load(p, u, tile0, col, grp);
-    // Normalisers of the lane's rows (tile0 + k)*16 + 4*grp + i.
-    float rmax[RTW][4], rinv[RTW][4];
-#pragma unroll
-    for (int k = 0; k < RTW; ++k) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = (tile0 + k) * 16 + 4 * grp + i;
-        const bool in = (tile0 + k) < row_tiles;
-        const float *st = p.row_stat + (u.ounit * p.rows_pad + (in ? r : 0)) * 2;
-        rmax[k][i] = in ? st[0] : INFINITY;
-        rinv[k][i] = in ? st[1] : 0.f;
-      }
+    // Normalisers of this group's rows, staged in LDS (absent rows: +inf, 0).
+    for (int i = threadIdx.x; i < kWaves * RTW * 16; i += kThreads) {
+      const int r = tg * 16 + i;
+      const bool in = r < p.rows_pad;
+      const float *st = p.row_stat + (u.ounit * p.rows_pad + (in ? r : 0)) * 2;
+      s_max[i] = in ? st[0] : INFINITY;
+      s_inv[i] = in ? st[1] : 0.f;
     }
+    const float *smax = s_max + wave * RTW * 16;
+    const float *sinv = s_inv + wave * RTW * 16;
     BlockRegs<T, D> regs;
     load_block<T, D>(regs, kbase, k0, u.L);
     int buf = 0;
@@ -322,9 +327,9 @@ __global__ __launch_bounds__(kThreads) void score_mass_kernel(ScoreParams p) {
       if (kb + kBlock < k1) load_block<T, D>(regs, kbase, kb + kBlock, u.L);
       float acc[2] = {0.f, 0.f};
       if (kb + kBlock <= full_end)
-        mass_block<T, D, RTW, true>(p, u, rb, stage[buf], kb, tile0, col, grp, rmax, rinv, acc);
+        mass_block<T, D, RTW, true>(p, u, rb, stage[buf], kb, tile0, col, grp, smax, sinv, acc);
       else
-        mass_block<T, D, RTW, false>(p, u, rb, stage[buf], kb, tile0, col, grp, rmax, rinv, acc);
+        mass_block<T, D, RTW, false>(p, u, rb, stage[buf], kb, tile0, col, grp, smax, sinv, acc);
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
         const float tot = group4_sum(acc[kt]);

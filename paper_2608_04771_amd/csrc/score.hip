@@ -141,38 +141,66 @@ __device__ __forceinline__ void key_frags(const unsigned char *stage, int kt, in
 
 // Statistics pass body for one 32-key block (two 16-key tiles): S^T = K.Q^T,
 // lane holds keys kb + kt*16 + 4*grp + i of row (tile0 + k)*16 + col; online
-// (max, sum) per lane, merged over the lane groups at the end of the chunk.
+// (max, sum) per lane over its 8 keys of the block at once (one rescale per
+// block), merged over the lane groups at the end of the chunk.  With a
+// positive scale the maximum is taken on the raw products and each term is
+// one fused multiply-add into the exponent.
 template <typename T, int D, int RTW, bool FULL>
 __device__ __forceinline__ void stats_block(const ScoreParams &p, const UnitInfo &u, const RowBlock<T, D, RTW> &rb,
                                             const unsigned char *stage, int kb, int col, int grp,
                                             float (&m)[RTW], float (&z)[RTW]) {
   using MF = Mfma<T>;
   using Cfg = ScoreCfg<T, D>;
+  typename MF::frag kf[2][Cfg::steps];
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt) {
-    typename MF::frag kf[Cfg::steps];
-    key_frags<T, D>(stage, kt, col, grp, kf);
+  for (int kt = 0; kt < 2; ++kt) key_frags<T, D>(stage, kt, col, grp, kf[kt]);
+  const float c = p.scale_log2;
 #pragma unroll
-    for (int k = 0; k < RTW; ++k) {
-      f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < RTW; ++k) {
+    f32x4_t s[2];
 #pragma unroll
-      for (int c = 0; c < Cfg::steps; ++c) s = MF::mma(kf[c], rb.q[k][c], s);
-      float x[4];
+    for (int kt = 0; kt < 2; ++kt) {
+      s[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < Cfg::steps; ++st) s[kt] = MF::mma(kf[kt][st], rb.q[k][st], s[kt]);
+    }
+    float v[8];
+    bool vis[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      v[e] = s[e >> 2][e & 3];
+      if constexpr (FULL) {
+        vis[e] = true;
+      } else {
+        const int key = kb + (e >> 2) * 16 + 4 * grp + (e & 3);
+        vis[e] = key < u.L && (!p.causal || key <= rb.pos[k]);
+      }
+    }
+    if (c > 0.f) {
+      float vmax = -INFINITY;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vmax = fmaxf(vmax, vis[e] ? v[e] : -INFINITY);
+      const float mn = fmaxf(m[k], vmax * c);
+      if (FULL || mn != -INFINITY) {
+        float sum = z[k] * fast_exp2(m[k] - mn);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sum += vis[e] ? fast_exp2(fmaf(v[e], c, -mn)) : 0.f;
+        z[k] = sum;
+        m[k] = mn;
+      }
+    } else {
+      float x[8];
       float tmax = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        x[i] = s[i] * p.scale_log2;
-        if constexpr (!FULL) {
-          const int key = kb + kt * 16 + 4 * grp + i;
-          x[i] = (key < u.L && (!p.causal || key <= rb.pos[k])) ? x[i] : -INFINITY;
-        }
-        tmax = fmaxf(tmax, x[i]);
+      for (int e = 0; e < 8; ++e) {
+        x[e] = vis[e] ? v[e] * c : -INFINITY;
+        tmax = fmaxf(tmax, x[e]);
       }
       const float mn = fmaxf(m[k], tmax);
       if (FULL || mn != -INFINITY) {
         float sum = z[k] * fast_exp2(m[k] - mn);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) sum += fast_exp2(x[i] - mn);
+        for (int e = 0; e < 8; ++e) sum += fast_exp2(x[e] - mn);
         z[k] = sum;
         m[k] = mn;
       }
@@ -181,7 +209,7 @@ __device__ __forceinline__ void stats_block(const ScoreParams &p, const UnitInfo
 }
 
 template <typename T, int D, int RTW>
-__global__ __launch_bounds__(kThreads) void score_stats_kernel(ScoreParams p) {
+__global__ __launch_bounds__(kThreads, 2) void score_stats_kernel(ScoreParams p) {
   constexpr int n_waves = kWaves;
   using Cfg = ScoreCfg<T, D>;
   using RB = RowBlock<T, D, RTW>;

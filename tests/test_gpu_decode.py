@@ -135,3 +135,25 @@ def test_decode_single_unit_max_splits(dtype, D, G):
     assert_lse_close(lse[0, 0], rl, dtype, "single unit")
     assert int(cache.length[0, 0, 0].item()) == n + 1
     assert torch.equal(cache.k[0, 0, 0, n].cpu(), kn[0, 0, 0]) and torch.equal(cache.v[0, 0, 0, n].cpu(), vn[0, 0, 0])
+
+
+@pytest.mark.parametrize("dtype,D", [("bf16", 128), ("f32", 64)])
+def test_decode_empty_unit_without_append(dtype, D):
+    """A unit with no rows and no append: output 0, lse -inf, statistics
+    (-inf, 0), as the header states; the other units are unaffected."""
+    NL, Bsz, H, Cap, G = 1, 1, 2, 64, 4
+    k, v, ln = _random_cache(NL, Bsz, H, Cap, D, dtype, [0, 40], seed=3)
+    q = torch.randn((NL, Bsz, H * G, D), generator=torch.Generator().manual_seed(4)).to(k.dtype)
+    cache = B.KVCache(k.cuda(), v.cuda(), ln.cuda())
+    st = torch.empty((NL, Bsz, H * G, 2), dtype=torch.float32, device="cuda")
+    dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out, lse = B.reco_decode_attn(cache, q.cuda(), dev_err=dev_err, row_stats=st)
+    torch.cuda.synchronize()
+    assert dev_err.item() == 0
+    assert (out[0, 0, :G].float() == 0).all()
+    assert torch.isinf(lse[0, 0, :G]).all() and (lse[0, 0, :G] < 0).all()
+    assert torch.isinf(st[0, 0, :G, 0]).all() and (st[0, 0, :G, 1] == 0).all()
+    ref, rl = oracle.decode_unit(f64(k[0, 0, 1][:40]), f64(v[0, 0, 1][:40]), 40, f64(q[0, 0, G:]), 1 / math.sqrt(D))
+    assert_decode_close(out[0, 0, G:], ref, dtype, "non-empty unit")
+    assert_lse_close(lse[0, 0, G:], rl, dtype, "non-empty unit")
+    assert cache.length.cpu().tolist() == [[[0, 40]]]

@@ -23,7 +23,8 @@ def _random_cache(NL, Bsz, H, Cap, D, dtype, lens, seed):
 
 
 @pytest.mark.parametrize("dtype,D,G", [("f32", 64, 4), ("f32", 128, 7), ("bf16", 128, 7), ("bf16", 64, 4),
-                                       ("bf16", 128, 1), ("bf16", 128, 16), ("f32", 64, 5), ("bf16", 128, 8)])
+                                       ("bf16", 128, 1), ("bf16", 128, 16), ("f32", 64, 5), ("bf16", 128, 8),
+                                       ("f32", 128, 16), ("bf16", 64, 16)])
 @pytest.mark.parametrize("append", [False, True])
 def test_decode_ragged_units(dtype, D, G, append):
     """Ragged per-unit lengths spanning empty, single-row, tile edges and a

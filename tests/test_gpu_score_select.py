@@ -45,7 +45,8 @@ def test_score_tiny_workload():
 
 @pytest.mark.parametrize("dtype,D,G,w", [("bf16", 128, 7, 64), ("bf16", 128, 5, 32), ("f32", 128, 4, 16),
                                          ("bf16", 64, 1, 8), ("bf16", 128, 8, 100),
-                                         ("bf16", 64, 16, 256)])                 # G*w = 4096 rows, the limit
+                                         ("bf16", 64, 16, 256),                  # G*w = 4096 rows, the limit
+                                         ("f32", 64, 16, 256), ("f32", 128, 8, 64)])
 @pytest.mark.parametrize("causal", [True, False])
 def test_score_ragged(dtype, D, G, w, causal):
     H, NL, Bsz = 2, 2, 2

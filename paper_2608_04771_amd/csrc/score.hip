@@ -33,6 +33,18 @@ constexpr int kThreads = 256;
 constexpr int kWaves = 4;       // waves per scoring workgroup
 constexpr int kBlock = 32;        // keys per LDS block (two 16-key MFMA tiles)
 
+// Sum over the four lanes {l, l^16, l^32, l^48} without an LDS round trip:
+// gfx950's row swaps hand each lane its partner row's value (rows 0/1 and
+// 2/3 for the 16-lane swap, 0/2 and 1/3 for the 32-lane swap), so two
+// butterfly steps leave the group's total in every lane.  Each step adds the
+// same two values as a shuffle-based butterfly, so the result is the same.
+__device__ __forceinline__ float group4_sum_swap(float v) {
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+}
+
 struct UnitInfo {
   int lc, b, h;
   size_t cunit;   // unit index in the whole cache
@@ -268,30 +280,33 @@ __global__ __launch_bounds__(kThreads, 2) void score_stats_kernel(ScoreParams p)
 
 // Mass pass body for one 32-key block: S = Q.K^T, lane holds rows
 // (tile0 + k)*16 + 4*grp + i of key kb + kt*16 + col, so the lane sums its
-// rows in registers and only the four lane groups meet at the end.
+// rows in registers and only the four lane groups meet at the end.  Both
+// 16-key tiles are processed per row tile, so each row tile's normalisers are
+// read from LDS once per block; each key's sum still runs over the rows in
+// the same order.
 template <typename T, int D, int RTW, bool FULL>
 __device__ __forceinline__ void mass_block(const ScoreParams &p, const UnitInfo &u, const RowBlock<T, D, RTW> &rb,
                                            const unsigned char *stage, int kb, int tile0, int col, int grp,
                                            const float *smax, const float *sinv, float (&acc)[2]) {
   using MF = Mfma<T>;
   using Cfg = ScoreCfg<T, D>;
+  typename MF::frag kf[2][Cfg::steps];
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt) {
-    typename MF::frag kf[Cfg::steps];
-    key_frags<T, D>(stage, kt, col, grp, kf);
-    const int key = kb + kt * 16 + col;
+  for (int kt = 0; kt < 2; ++kt) key_frags<T, D>(stage, kt, col, grp, kf[kt]);
 #pragma unroll
-    for (int k = 0; k < RTW; ++k) {
+  for (int k = 0; k < RTW; ++k) {
+    const float4 mx = *reinterpret_cast<const float4 *>(smax + k * 16 + 4 * grp);
+    const float4 iv = *reinterpret_cast<const float4 *>(sinv + k * 16 + 4 * grp);
+    const float rmax[4] = {mx.x, mx.y, mx.z, mx.w};
+    const float rinv[4] = {iv.x, iv.y, iv.z, iv.w};
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      const int key = kb + kt * 16 + col;
       f32x4_t s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int c = 0; c < Cfg::steps; ++c) s = MF::mma(rb.q[k][c], kf[c], s);
-      const float4 mx = *reinterpret_cast<const float4 *>(smax + k * 16 + 4 * grp);
-      const float4 iv = *reinterpret_cast<const float4 *>(sinv + k * 16 + 4 * grp);
-      const float rmax[4] = {mx.x, mx.y, mx.z, mx.w};
-      const float rinv[4] = {iv.x, iv.y, iv.z, iv.w};
+      for (int c = 0; c < Cfg::steps; ++c) s = MF::mma(rb.q[k][c], kf[kt][c], s);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        // Absent rows carry max = +inf and 1/sum = 0, so they add exactly 0.
         const float e = fast_exp2(fmaf(s[i], p.scale_log2, -rmax[i]));
         if constexpr (FULL) {
           acc[kt] = fmaf(e, rinv[i], acc[kt]);
@@ -330,8 +345,6 @@ __global__ __launch_bounds__(kThreads, 2) void score_mass_kernel(ScoreParams p) 
   const int row_tiles = p.rows_pad / 16;
   const int full_end = p.causal ? min(u.L, u.L - p.w + 1) : u.L;
 
-  for (int i = threadIdx.x; i < n_waves * kScoreChunk; i += kThreads) (&part[0][0])[i] = 0.f;
-
   for (int tg = 0; tg < row_tiles; tg += n_waves * RTW) {
     const int tile0 = tg + wave * RTW;
     RB rb;
@@ -360,8 +373,12 @@ __global__ __launch_bounds__(kThreads, 2) void score_mass_kernel(ScoreParams p) 
         mass_block<T, D, RTW, false>(p, u, rb, stage[buf], kb, tile0, col, grp, smax, sinv, acc);
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
-        const float tot = group4_sum(acc[kt]);
-        if (grp == 0) part[wave][kb - k0 + kt * 16 + col] += tot;
+        const float tot = group4_sum_swap(acc[kt]);
+        if (grp == 0) {
+          // The first row group writes every column sum the final loop reads.
+          if (tg == 0) part[wave][kb - k0 + kt * 16 + col] = tot;
+          else part[wave][kb - k0 + kt * 16 + col] += tot;
+        }
       }
     }
     __syncthreads();   // the stage is reused by the next row-tile group

@@ -210,7 +210,8 @@ reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int
  * reward[b] >= tau_hi, beta_mid otherwise (fp32 comparisons), and
  * logits[b][u] -= beta_b (one fp32 subtraction) for every DISTINCT id u in
  * refl_ids.  All other logits are untouched (bit-exact).
- *   logits   : [rows][ld] fp32, in place; ld >= vocab
+ *   logits   : [rows][ld] fp32, in place; ld >= vocab; 1 <= vocab <= 2^30
+ *              (larger: RECO_ERR_UNSUPPORTED); 1 <= rows <= 65535
  *   refl_ids : [n_refl] int32, 0 <= n_refl <= 4096, each in [0, vocab)
  *   reward   : [rows] fp32
  * An id outside [0, vocab) is skipped and sets RECO_DEV_BAD_TOKEN_ID. */
@@ -232,7 +233,7 @@ reco_status_t reco_logit_penalty(float *logits, int32_t rows, int32_t vocab, int
  *            counter (u / 4, b, offset low, offset high), key (seed low,
  *            seed high).  (seed, offset, b, u) fixes the draw: advance
  *            `offset` once per generated token for fresh noise.
- *   logits   : [rows][ld] fp32, in place; ld >= vocab
+ *   logits   : [rows][ld] fp32, in place; ld >= vocab; 1 <= vocab <= 2^30
  *   refl_ids : [n_refl] int32, 0 <= n_refl <= 4096 (nullable when 0)
  *   reward   : [rows] fp32
  *   tokens   : [rows] int32 (output)
@@ -253,9 +254,11 @@ reco_status_t reco_penalty_sample(float *logits, int32_t rows, int32_t vocab, in
  * every sequence b, ppl[b] = exp((1/n) sum_t (LSE(logits[b][t]) -
  * logits[b][t][tokens[b][t]])) with natural logarithms, and
  * stop[b] = (ppl[b] <= tau_p).
- *   logits : [batch][n][vocab] fp32 (the probe answer's raw logits)
+ *   logits : [batch][n][vocab] fp32 (the probe answer's raw logits),
+ *            1 <= vocab <= 2^30 (larger: RECO_ERR_UNSUPPORTED)
  *   tokens : [batch][n] int32 in [0, vocab)
  *   ppl    : [batch] fp32 (output);  stop : nullable [batch] int32 (output)
+ *   batch * n <= 65535 (larger: RECO_ERR_UNSUPPORTED)
  * Row log-sum-exps are fp32 partials merged in fp64.  A token out of range
  * makes ppl NaN for its sequence and sets RECO_DEV_BAD_TOKEN_ID. */
 size_t reco_answer_ppl_workspace_size(int32_t batch, int32_t n, int32_t vocab);

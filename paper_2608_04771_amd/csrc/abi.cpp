@@ -12,6 +12,10 @@
 
 namespace {
 
+// Largest vocabulary the logit kernels take: chunk ends (start + chunk
+// length) and row offsets then stay far inside int32.
+constexpr int32_t kMaxVocab = 1 << 30;
+
 bool cache_ok(const reco_kv_cache_t *c) {
   return c && c->k && c->v && c->len && c->n_layers >= 1 && c->batch >= 1 && c->n_kv_heads >= 1 &&
          c->capacity >= 1;
@@ -98,9 +102,9 @@ int32_t reco_kept_count(int32_t L, int32_t w, double r) {
 
 // ---------------------------------------------------------------- score
 size_t reco_score_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers, int32_t n_q_heads, int32_t w) {
-  if (!cache_ok(cache) || n_layers < 1 || w < 1) return 0;
+  if (!cache_ok(cache) || !units_ok(cache, n_layers) || w < 1) return 0;
   const int G = group_of(cache, n_q_heads);
-  if (G < 1) return 0;
+  if (G < 1 || static_cast<int64_t>(G) * w > reco::kScoreMaxRows) return 0;
   const int units = n_layers * cache->batch * cache->n_kv_heads;
   return reco::score_workspace_bytes(units, cache->capacity, G * w);
 }
@@ -148,7 +152,7 @@ reco_status_t reco_score(const reco_kv_cache_t *cache, int32_t layer0, int32_t n
 
 // ---------------------------------------------------------------- select + compact
 size_t reco_select_compact_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers) {
-  if (!cache_ok(cache) || n_layers < 1) return 0;
+  if (!cache_ok(cache) || !units_ok(cache, n_layers)) return 0;
   const int units = n_layers * cache->batch * cache->n_kv_heads;
   return reco::select_workspace_bytes(units, cache->capacity, true);
 }
@@ -216,7 +220,7 @@ reco_status_t reco_pool_scores(const reco_kv_cache_t *cache, int32_t layer0, int
 
 // ---------------------------------------------------------------- decode
 size_t reco_decode_attn_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers, int32_t n_q_heads) {
-  if (!cache_ok(cache) || n_layers < 1 || group_of(cache, n_q_heads) < 1) return 0;
+  if (!cache_ok(cache) || !units_ok(cache, n_layers) || group_of(cache, n_q_heads) < 1) return 0;
   const int units = n_layers * cache->batch * cache->n_kv_heads;
   return reco::decode_workspace_bytes(units, cache->capacity, cache->head_dim);
 }
@@ -268,6 +272,7 @@ reco_status_t reco_logit_penalty(float *logits, int32_t rows, int32_t vocab, int
                                  int32_t n_refl, const float *reward, float tau_lo, float tau_hi, float beta_lo,
                                  float beta_mid, float beta_hi, int32_t *dev_err, hipStream_t stream) {
   if (!logits || !reward || rows < 1 || rows > 65535 || vocab < 1 || ld < vocab) return RECO_ERR_INVALID_ARG;
+  if (vocab > kMaxVocab) return RECO_ERR_UNSUPPORTED;
   if (n_refl < 0 || n_refl > 4096 || (n_refl > 0 && !refl_ids)) return RECO_ERR_INVALID_ARG;
   if (n_refl == 0) return RECO_OK;
   return hip_status(reco::launch_logit_penalty(logits, rows, vocab, ld, refl_ids, n_refl, reward, tau_lo, tau_hi,
@@ -276,7 +281,7 @@ reco_status_t reco_logit_penalty(float *logits, int32_t rows, int32_t vocab, int
 
 // ---------------------------------------------------------------- penalty + sampling
 size_t reco_penalty_sample_workspace_size(int32_t rows, int32_t vocab) {
-  if (rows < 1 || vocab < 1) return 0;
+  if (rows < 1 || vocab < 1 || vocab > kMaxVocab) return 0;
   return reco::penalty_sample_workspace_bytes(rows, vocab);
 }
 
@@ -288,6 +293,7 @@ reco_status_t reco_penalty_sample(float *logits, int32_t rows, int32_t vocab, in
     return RECO_ERR_INVALID_ARG;
   if (n_refl < 0 || n_refl > 4096 || (n_refl > 0 && !refl_ids)) return RECO_ERR_INVALID_ARG;
   if (!(temperature >= 0.f) || !isfinite(temperature)) return RECO_ERR_INVALID_ARG;
+  if (vocab > kMaxVocab) return RECO_ERR_UNSUPPORTED;
   const size_t need = reco::penalty_sample_workspace_bytes(rows, vocab);
   if (!ws || ws_bytes < need) return RECO_ERR_WORKSPACE;
   return hip_status(reco::launch_penalty_sample(logits, rows, vocab, ld, refl_ids, n_refl, reward, tau_lo, tau_hi,
@@ -297,7 +303,7 @@ reco_status_t reco_penalty_sample(float *logits, int32_t rows, int32_t vocab, in
 
 // ---------------------------------------------------------------- answer PPL
 size_t reco_answer_ppl_workspace_size(int32_t batch, int32_t n, int32_t vocab) {
-  if (batch < 1 || n < 1 || vocab < 1) return 0;
+  if (batch < 1 || n < 1 || vocab < 1 || vocab > kMaxVocab) return 0;
   return reco::ppl_workspace_bytes(batch, n, vocab);
 }
 
@@ -305,6 +311,7 @@ reco_status_t reco_answer_ppl(const float *logits, const int32_t *tokens, int32_
                               float tau_p, float *ppl, int32_t *stop, void *ws, size_t ws_bytes, int32_t *dev_err,
                               hipStream_t stream) {
   if (!logits || !tokens || !ppl || batch < 1 || n < 1 || vocab < 1) return RECO_ERR_INVALID_ARG;
+  if (vocab > kMaxVocab) return RECO_ERR_UNSUPPORTED;
   if (batch > 65535 || static_cast<int64_t>(batch) * n > 65535) return RECO_ERR_UNSUPPORTED;
   const size_t need = reco::ppl_workspace_bytes(batch, n, vocab);
   if (!ws || ws_bytes < need) return RECO_ERR_WORKSPACE;

@@ -296,7 +296,7 @@ hipError_t launch_logit_penalty(float *logits, int rows, int vocab, int64_t ld, 
 }
 
 size_t penalty_sample_workspace_bytes(int rows, int vocab) {
-  const size_t chunks = static_cast<size_t>((vocab + kSmpChunk - 1) / kSmpChunk);
+  const size_t chunks = static_cast<size_t>((static_cast<int64_t>(vocab) + kSmpChunk - 1) / kSmpChunk);
   return static_cast<size_t>(rows) * chunks * sizeof(SamplePart);
 }
 
@@ -304,7 +304,7 @@ hipError_t launch_penalty_sample(float *logits, int rows, int vocab, int64_t ld,
                                  const float *reward, float tau_lo, float tau_hi, float b_lo, float b_mid,
                                  float b_hi, float temperature, uint64_t seed, uint64_t offset, int32_t *tokens,
                                  void *ws, int32_t *dev_err, hipStream_t s) {
-  const int chunks = (vocab + kSmpChunk - 1) / kSmpChunk;
+  const int chunks = static_cast<int>((static_cast<int64_t>(vocab) + kSmpChunk - 1) / kSmpChunk);
   SamplePart *part = reinterpret_cast<SamplePart *>(ws);
   hipLaunchKernelGGL(penalty_sample_partial_kernel, dim3(chunks, rows), dim3(kSmpThreads), 0, s, logits, vocab, ld,
                      ids, n_ids, reward, tau_lo, tau_hi, b_lo, b_mid, b_hi, temperature,
@@ -319,13 +319,13 @@ hipError_t launch_penalty_sample(float *logits, int rows, int vocab, int64_t ld,
 }
 
 size_t ppl_workspace_bytes(int batch, int n, int vocab) {
-  const size_t chunks = static_cast<size_t>((vocab + kPplChunk - 1) / kPplChunk);
+  const size_t chunks = static_cast<size_t>((static_cast<int64_t>(vocab) + kPplChunk - 1) / kPplChunk);
   return static_cast<size_t>(batch) * n * chunks * 2 * sizeof(float);
 }
 
 hipError_t launch_answer_ppl(const float *logits, const int32_t *tokens, int batch, int n, int vocab, float tau_p,
                              float *ppl, int32_t *stop, void *ws, int32_t *dev_err, hipStream_t s) {
-  const int chunks = (vocab + kPplChunk - 1) / kPplChunk;
+  const int chunks = static_cast<int>((static_cast<int64_t>(vocab) + kPplChunk - 1) / kPplChunk);
   float *part = reinterpret_cast<float *>(ws);
   hipLaunchKernelGGL(ppl_partial_kernel, dim3(chunks, batch * n), dim3(kPplThreads), 0, s, logits, vocab, chunks,
                      part);

@@ -178,6 +178,7 @@ def test_penalty_and_ppl_reject_bad_arguments():
     assert pen(n=5000) == B.RECO_ERR_INVALID_ARG
     assert pen(rew=0) == B.RECO_ERR_INVALID_ARG
     assert pen(n=0, ids=0) == B.RECO_OK                                   # empty set: nothing to do
+    assert pen(vocab=(1 << 30) + 1, ld=(1 << 30) + 1) == B.RECO_ERR_UNSUPPORTED
     ppl = lambda logits=0x10, tok=0x20, b=2, n=4, v=100, out=0x30, ws=0x40, wsb=1 << 20: lib.reco_answer_ppl(  # noqa: E731
         P(logits), P(tok), b, n, v, 1.1, P(out), None, P(ws), wsb, None, None)
     assert ppl(logits=0) == B.RECO_ERR_INVALID_ARG
@@ -185,6 +186,8 @@ def test_penalty_and_ppl_reject_bad_arguments():
     assert ppl(out=0) == B.RECO_ERR_INVALID_ARG
     assert ppl(ws=0) == B.RECO_ERR_WORKSPACE
     assert ppl(wsb=4) == B.RECO_ERR_WORKSPACE
+    assert ppl(v=(1 << 30) + 1) == B.RECO_ERR_UNSUPPORTED
+    assert ppl(b=300, n=300) == B.RECO_ERR_UNSUPPORTED                  # batch * n > 65535
 
 
 def test_penalty_sample_rejects_bad_arguments():
@@ -209,6 +212,7 @@ def test_penalty_sample_rejects_bad_arguments():
         assert smp(T=bad_t) == B.RECO_ERR_INVALID_ARG, bad_t
     assert smp(ws=0) == B.RECO_ERR_WORKSPACE
     assert smp(wsb=need - 1) == B.RECO_ERR_WORKSPACE
+    assert smp(vocab=(1 << 30) + 1, ld=(1 << 30) + 1, wsb=1 << 40) == B.RECO_ERR_UNSUPPORTED
 
 
 def test_workspace_sizes_are_positive_and_monotone():
@@ -221,3 +225,21 @@ def test_workspace_sizes_are_positive_and_monotone():
         assert 0 < a <= b, fn
     assert lib.reco_answer_ppl_workspace_size(8, 32, 152064) >= 8 * 32 * 2 * 4
     assert lib.reco_answer_ppl_workspace_size(0, 32, 10) == 0
+
+
+def test_workspace_sizes_reject_shapes_the_calls_reject():
+    """Sizes are 0 (never an overflowed number) for shapes the entry points
+    refuse: too many units for one grid dimension, G * w beyond the score's
+    row limit, a vocabulary beyond 2^30."""
+    lib = B.load_library()
+    many = _fake_cache(batch=40000, n_kv_heads=2)                        # 80,000 units per layer
+    assert lib.reco_score_workspace_size(ctypes.byref(many), 1, 2, 8) == 0
+    assert lib.reco_decode_attn_workspace_size(ctypes.byref(many), 1, 2) == 0
+    assert lib.reco_select_compact_workspace_size(ctypes.byref(many), 1) == 0
+    ok = _fake_cache(capacity=100000)
+    assert lib.reco_score_workspace_size(ctypes.byref(ok), 2, 2 * 64, 64) > 0      # G*w = 4096, the limit
+    assert lib.reco_score_workspace_size(ctypes.byref(ok), 2, 2 * 65, 64) == 0     # 4160 rows
+    assert lib.reco_score_workspace_size(ctypes.byref(ok), 2, 2, 2 ** 31 - 1) == 0
+    assert lib.reco_penalty_sample_workspace_size(3, 1 << 30) >= 3 * (1 << 20) * 8
+    assert lib.reco_penalty_sample_workspace_size(3, 2 ** 31 - 1) == 0
+    assert lib.reco_answer_ppl_workspace_size(1, 1, 2 ** 31 - 1) == 0

@@ -16,7 +16,9 @@
 // log2 domain with fp32 statistics.  The four waves' (max, sum, O) states are
 // merged through LDS and written as one split partial.  A second kernel
 // merges the splits of each unit, writes out / lse and commits the optional
-// append (so no workgroup of the attention kernel races on len).  Merging in
+// append (so no workgroup of the attention kernel races on len); a unit
+// covered by a single workgroup (one split) is finalised by that workgroup,
+// with no second launch.  Merging in
 // the last-finishing workgroup instead would need device-scope fences, which
 // on this chip write back and invalidate the L2 that the streaming
 // workgroups depend on.
@@ -161,8 +163,8 @@ __global__ __launch_bounds__(kThreads, (DecodeCfg<T, D>::min_wgs)) void decode_s
   const size_t cunit = (static_cast<size_t>(p.layer0 + lc) * p.batch + b) * p.hkv + h;
   const size_t qunit = static_cast<size_t>(lc) * per_layer + static_cast<size_t>(b) * p.hkv + h;
 
-  int n_cache = p.len[cunit];
-  n_cache = n_cache < 0 ? 0 : (n_cache > p.cap ? p.cap : n_cache);
+  const int len_in = p.len[cunit];
+  const int n_cache = len_in < 0 ? 0 : (len_in > p.cap ? p.cap : len_in);
   const bool append = p.k_new != nullptr;
   const int n_tot = n_cache + (append ? 1 : 0);
   const T *kbase = reinterpret_cast<const T *>(p.k) + cunit * p.cap * D;
@@ -297,6 +299,52 @@ __global__ __launch_bounds__(kThreads, (DecodeCfg<T, D>::min_wgs)) void decode_s
     for (int i = 0; i < 4; ++i) ow[(wave * 16 + col) * D + dt * 16 + 4 * grp + i] = o[dt][i];
   }
   __syncthreads();
+
+  if (p.splits == 1) {
+    // The workgroup holds its unit's whole softmax: it writes out / lse /
+    // row_stats and commits the append itself, with the arithmetic of the
+    // merge of a single split (weight exp2(0) * 1/L, added to zero).
+    const size_t oq0 = (static_cast<size_t>(lc) * p.batch + b) * p.hq + h * p.group;
+    for (int idx = threadIdx.x; idx < p.group * D; idx += kThreads) {
+      const int qi = idx / D;
+      const int d = idx - qi * D;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < kWavesPerWG; ++w) M = fmaxf(M, mw[w * 16 + qi]);
+      float acc = 0.f, L = 0.f;
+      if (M != -INFINITY) {
+#pragma unroll
+        for (int w = 0; w < kWavesPerWG; ++w) {
+          const float e = fast_exp2(mw[w * 16 + qi] - M);
+          acc += ow[(w * 16 + qi) * D + d] * e;
+          L += lw[w * 16 + qi] * e;
+        }
+      }
+      const float inv = L > 0.f ? 1.f / L : 0.f;
+      reinterpret_cast<T *>(p.out)[(oq0 + qi) * D + d] = from_f32<T>(fmaf(acc, inv, 0.f));
+      if (d == 0) {
+        if (p.lse) p.lse[oq0 + qi] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+        if (p.row_stats) {
+          p.row_stats[(oq0 + qi) * 2 + 0] = M;
+          p.row_stats[(oq0 + qi) * 2 + 1] = L;
+        }
+      }
+    }
+    // Every wave has finished reading the cache (barrier above); row n_cache
+    // is read by no one in this call (the new key comes from k_new).
+    if (threadIdx.x == 0 && (len_in < 0 || len_in > p.cap)) report(p.dev_err, 5 /*RECO_DEV_BAD_LENGTH*/);
+    if (!append || len_in < 0 || len_in > p.cap) return;
+    if (len_in == p.cap) {
+      if (threadIdx.x == 0) report(p.dev_err, 1 /*RECO_DEV_APPEND_OVERFLOW*/);
+      return;
+    }
+    for (int d = threadIdx.x; d < D; d += kThreads) {
+      reinterpret_cast<T *>(p.k)[(cunit * p.cap + len_in) * D + d] = knew[d];
+      reinterpret_cast<T *>(p.v)[(cunit * p.cap + len_in) * D + d] = vnew[d];
+    }
+    if (threadIdx.x == 0) p.len[cunit] = len_in + 1;
+    return;
+  }
 
   const size_t pbase = static_cast<size_t>(unit) * p.splits + split;
   float *po = p.part_o + pbase * 16 * D;
@@ -543,7 +591,7 @@ hipError_t launch_typed(const DecodeParams &p, hipStream_t s) {
   const int units = p.n_layers * p.batch * p.hkv;
   hipLaunchKernelGGL((decode_split_kernel<T, D>), dim3(p.splits, units), dim3(kThreads), 0, s, p);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || p.splits == 1) return e;   // one split: finalised in place
   if (p.splits >= kWideMinSplits)
     hipLaunchKernelGGL((decode_merge_wide_kernel<T, D>), dim3(units, p.group), dim3(kWideThreads), 0, s, p);
   else

@@ -158,3 +158,42 @@ def test_decode_empty_unit_without_append(dtype, D):
     assert_decode_close(out[0, 0, G:], ref, dtype, "non-empty unit")
     assert_lse_close(lse[0, 0, G:], rl, dtype, "non-empty unit")
     assert cache.length.cpu().tolist() == [[[0, 40]]]
+
+
+@pytest.mark.parametrize("cap", [64, 512, 4096])
+def test_decode_bad_length_is_reported(cap):
+    """A stored length below 0 or above capacity sets RECO_DEV_BAD_LENGTH; the
+    unit attends over its clamped rows (plus the new token), performs no
+    append and keeps its length.  The capacities cover the three completion
+    paths: one split finalised in place (64), the one-wave merge of a few
+    splits (512) and the many-split merge (4096)."""
+    NL, Bsz, H, D, G = 1, 1, 3, 128, 4
+    lens = [-3, cap + 5, 20]
+    g = torch.Generator().manual_seed(cap)
+    k = torch.randn((NL, Bsz, H, cap, D), generator=g).to(torch.bfloat16)
+    v = torch.randn((NL, Bsz, H, cap, D), generator=g).to(torch.bfloat16)
+    q = torch.randn((NL, Bsz, H * G, D), generator=g).to(torch.bfloat16)
+    kn = torch.randn((NL, Bsz, H, D), generator=g).to(torch.bfloat16)
+    vn = torch.randn((NL, Bsz, H, D), generator=g).to(torch.bfloat16)
+    ln = torch.tensor(lens, dtype=torch.int32).reshape(NL, Bsz, H)
+    cache = B.KVCache(k.cuda(), v.cuda(), ln.cuda())
+    dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out, _ = B.reco_decode_attn(cache, q.cuda(), kn.cuda(), vn.cuda(), dev_err=dev_err)
+    torch.cuda.synchronize()
+    assert dev_err.item() == 5
+    assert cache.length.cpu().reshape(-1).tolist() == [-3, cap + 5, 21]
+    out = out.cpu()
+    scale = 1 / math.sqrt(D)
+    # length -3: no cached rows, so every head returns the new token's value
+    assert torch.equal(out[0, 0, :G], vn[0, 0, 0].expand(G, D))
+    # length cap + 5: the cap rows plus the new token
+    ref, _ = oracle.decode_unit(f64(k[0, 0, 1]), f64(v[0, 0, 1]), cap, f64(q[0, 0, G:2 * G]), scale,
+                                f64(kn[0, 0, 1]), f64(vn[0, 0, 1]))
+    assert_decode_close(out[0, 0, G:2 * G], ref, "bf16", f"cap={cap} clamped unit")
+    # the valid unit attends and appends as usual
+    ref, _ = oracle.decode_unit(f64(k[0, 0, 2]), f64(v[0, 0, 2]), 20, f64(q[0, 0, 2 * G:]), scale,
+                                f64(kn[0, 0, 2]), f64(vn[0, 0, 2]))
+    assert_decode_close(out[0, 0, 2 * G:], ref, "bf16", f"cap={cap} valid unit")
+    kc, vc = cache.k.cpu(), cache.v.cpu()
+    assert torch.equal(kc[0, 0, :2], k[0, 0, :2]) and torch.equal(vc[0, 0, :2], v[0, 0, :2])   # no append
+    assert torch.equal(kc[0, 0, 2, 20], kn[0, 0, 2]) and torch.equal(vc[0, 0, 2, 20], vn[0, 0, 2])

@@ -335,7 +335,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="7b16k", choices=sorted(I.WORKLOADS))
+    # The batch, 32B and trajectory workloads do not fit this bench's one
+    # pristine cache copy per step; the full-size GPU tests measure them.
+    ap.add_argument("--workload", default="7b16k", choices=["7b16k", "tiny"])
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
     ap.add_argument("--no-extras", dest="extras", action="store_false",
                     help="skip the measurements made after the timed steps (for profiler runs)")

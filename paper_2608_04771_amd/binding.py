@@ -94,7 +94,15 @@ def _ptr(t: Optional[torch.Tensor]):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+# torch's current-stream handle without building a Stream object (a few
+# microseconds per call otherwise); the public call is the fallback.
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
 def _stream(device) -> ctypes.c_void_p:
+    if _raw_stream is not None:
+        idx = device.index if device.index is not None else torch.cuda.current_device()
+        return ctypes.c_void_p(_raw_stream(idx))
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
@@ -165,16 +173,18 @@ def answer_ppl_workspace_size(batch: int, n: int, vocab: int) -> int:
     return int(load_library().reco_answer_ppl_workspace_size(batch, n, vocab))
 
 
-def _ws(nbytes: int, device, ws: Optional[torch.Tensor]) -> torch.Tensor:
+def _ws(nbytes, device, ws: Optional[torch.Tensor]) -> torch.Tensor:
+    """The caller's workspace, else a new one of nbytes() bytes (the library
+    checks the size either way)."""
     if ws is not None:
         return ws
-    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+    return torch.empty(max(int(nbytes()), 1), dtype=torch.uint8, device=device)
 
 
 def decode_workspace(cache: "KVCache", n_q_heads: int, n_layers: Optional[int] = None) -> torch.Tensor:
     """A decode workspace (contents need not be initialised).  Do not share
     one between overlapping calls."""
-    return _ws(decode_attn_workspace_size(cache, n_q_heads, n_layers), cache.k.device, None)
+    return _ws(lambda: decode_attn_workspace_size(cache, n_q_heads, n_layers), cache.k.device, None)
 
 
 def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[float] = None, causal: bool = True,
@@ -196,7 +206,7 @@ def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[floa
     if row_stats is not None and (row_stats.dtype != torch.float32 or tuple(row_stats.shape) != (nl, B, hq, w, 2)):
         raise ValueError("row_stats must be float32 [n_layers][B][Hq][w][2]")
     _need_cuda(q_win, scores, ws, dev_err, row_stats)
-    ws = _ws(score_workspace_size(cache, hq, w, nl), cache.k.device, ws)
+    ws = _ws(lambda: score_workspace_size(cache, hq, w, nl), cache.k.device, ws)
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     st = load_library().reco_score(cache.ref(), layer0, nl, _ptr(q_win), hq, w, scale,
                                    RECO_SCORE_CAUSAL if causal else 0, _ptr(row_stats), _ptr(scores), _ptr(ws),
@@ -227,7 +237,7 @@ def reco_select_compact(cache: KVCache, scores: torch.Tensor, retention: torch.T
     if kept_idx is not None and kept_idx.dtype != torch.int32:
         raise ValueError("kept_idx must be int32")
     _need_cuda(scores, retention, kept_idx, ws, dev_err)
-    ws = _ws(select_compact_workspace_size(cache, nl), cache.k.device, ws)
+    ws = _ws(lambda: select_compact_workspace_size(cache, nl), cache.k.device, ws)
     st = load_library().reco_select_compact(cache.ref(), layer0, nl, _ptr(scores), _ptr(retention), stride, w,
                                             _ptr(kept_idx), _ptr(ws), ws.numel(), _ptr(dev_err),
                                             _stream(cache.k.device))
@@ -275,7 +285,7 @@ def reco_decode_attn(cache: KVCache, q: torch.Tensor, k_new: Optional[torch.Tens
     if row_stats is not None and (row_stats.dtype != torch.float32 or tuple(row_stats.shape) != (nl, B, hq, 2)):
         raise ValueError("row_stats must be float32 [n_layers][B][Hq][2]")
     _need_cuda(q, k_new, v_new, out, lse, ws, dev_err, row_stats)
-    ws = _ws(decode_attn_workspace_size(cache, hq, nl), q.device, ws)
+    ws = _ws(lambda: decode_attn_workspace_size(cache, hq, nl), q.device, ws)
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     st = load_library().reco_decode_attn(cache.ref(), layer0, nl, _ptr(q), hq, scale, _ptr(k_new), _ptr(v_new),
                                          _ptr(out), _ptr(lse), _ptr(row_stats), _ptr(ws), ws.numel(), _ptr(dev_err),
@@ -322,7 +332,7 @@ def reco_penalty_sample(logits: torch.Tensor, refl_ids: Optional[torch.Tensor], 
     if tokens.dtype != torch.int32:
         raise ValueError("tokens must be int32")
     _need_cuda(refl_ids, reward, tokens, ws, dev_err)
-    ws = _ws(penalty_sample_workspace_size(rows, vocab), logits.device, ws)
+    ws = _ws(lambda: penalty_sample_workspace_size(rows, vocab), logits.device, ws)
     n_refl = 0 if refl_ids is None else refl_ids.numel()
     st = load_library().reco_penalty_sample(_ptr(logits), rows, vocab, logits.stride(0), _ptr(refl_ids), n_refl,
                                             _ptr(reward), tau_lo, tau_hi, beta_lo, beta_mid, beta_hi,
@@ -345,7 +355,7 @@ def reco_answer_ppl(logits: torch.Tensor, tokens: torch.Tensor, tau_p: float, pp
     if stop is None:
         stop = torch.empty(B, dtype=torch.int32, device=logits.device)
     _need_cuda(logits, tokens, ppl, stop, ws, dev_err)
-    ws = _ws(answer_ppl_workspace_size(B, n, V), logits.device, ws)
+    ws = _ws(lambda: answer_ppl_workspace_size(B, n, V), logits.device, ws)
     st = load_library().reco_answer_ppl(_ptr(logits), _ptr(tokens), B, n, V, tau_p, _ptr(ppl), _ptr(stop),
                                         _ptr(ws), ws.numel(), _ptr(dev_err), _stream(logits.device))
     _check(st, "reco_answer_ppl")

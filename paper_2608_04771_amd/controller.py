@@ -140,7 +140,9 @@ class RecoDecoder:
         dev = cache.k.device
         prompt_len = int(cache.length[0, 0, 0].item())
         self.sched = [RewardSchedule(policy, prompt_len, NL) for _ in range(Bsz)]
-        self.ring = prompt_q.clone()                      # row t % w holds the query of token t
+        # slot t % w holds the query of token t, [w][NL][B][Hq][D] (each slot
+        # contiguous, so a caller can write the next query straight into it)
+        self.ring = prompt_q.permute(3, 0, 1, 2, 4).contiguous()
         # slot t % w holds the (max, sum) decode statistics of token t, [w][NL][B][Hq][2]
         self.stats_ring = torch.zeros((w, NL, Bsz, n_q_heads, 2), dtype=torch.float32, device=dev)
         self.last_score_stats_fed = False
@@ -160,21 +162,30 @@ class RecoDecoder:
         self.lse = torch.empty((NL, Bsz, n_q_heads), dtype=torch.float32, device=dev)
         self.tokens = torch.empty(Bsz, dtype=torch.int32, device=dev)
         self.ws_smp = None
-        # Positions 0..prompt_len-1 are in the cache; the ring's rows hold
+        self.smp_shape = None                             # (rows, vocab) the sampling workspace was sized for
+        # Positions 0..prompt_len-1 are in the cache; the ring's slots hold
         # prompt positions prompt_len - w .. prompt_len - 1 in order, i.e. the
-        # row of position p is p % w once rotated into place.
+        # slot of position p is p % w once rotated into place.
         shift = prompt_len % w
         if shift:
-            self.ring = torch.roll(self.ring, shifts=shift, dims=3).contiguous()
+            self.ring = torch.roll(self.ring, shifts=shift, dims=0).contiguous()
+
+    def query_slot(self) -> torch.Tensor:
+        """The ring slot of the next token's query, [NL][B][Hq][D]: a caller
+        that writes the query here saves decode() the copy."""
+        return self.ring[self.count % self.policy.window]
 
     def decode(self, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
                logits: Optional[torch.Tensor] = None):
-        """One generated token: store its query in the window ring, attend
-        (appending its K/V) and apply the current reflection penalty to its
-        logit rows ([B][vocab], in place).  Returns (out, lse)."""
+        """One generated token: store its query in the window ring (no copy
+        when q is query_slot()), attend (appending its K/V) and apply the
+        current reflection penalty to its logit rows ([B][vocab], in place).
+        Returns (out, lse)."""
         w = self.policy.window
-        self.ring[:, :, :, self.count % w, :].copy_(q)
-        B.reco_decode_attn(self.cache, q, k_new, v_new, out=self.out, lse=self.lse, ws=self.ws_dec,
+        slot = self.ring[self.count % w]
+        if q.data_ptr() != slot.data_ptr():
+            slot.copy_(q)
+        B.reco_decode_attn(self.cache, slot, k_new, v_new, out=self.out, lse=self.lse, ws=self.ws_dec,
                            dev_err=self.dev_err, row_stats=self.stats_ring[self.count % w])
         if logits is not None and self.refl is not None:
             p = self.policy
@@ -194,9 +205,11 @@ class RecoDecoder:
         if self.refl is None:
             raise ValueError("sampling with the reflection penalty needs refl_ids")
         rows, vocab = logits.shape
-        need = B.penalty_sample_workspace_size(rows, vocab)
-        if self.ws_smp is None or self.ws_smp.numel() < need:
-            self.ws_smp = torch.empty(need, dtype=torch.uint8, device=logits.device)
+        if self.smp_shape != (rows, vocab):
+            need = B.penalty_sample_workspace_size(rows, vocab)
+            if self.ws_smp is None or self.ws_smp.numel() < need:
+                self.ws_smp = torch.empty(need, dtype=torch.uint8, device=logits.device)
+            self.smp_shape = (rows, vocab)
         p = self.policy
         return B.reco_penalty_sample(logits, self.refl, self.band_reward, p.tau_lo, p.tau_hi, *p.betas, temperature,
                                      seed, self.count, tokens=self.tokens, ws=self.ws_smp, dev_err=self.dev_err)
@@ -204,7 +217,7 @@ class RecoDecoder:
     def window_queries(self) -> torch.Tensor:
         """The last w queries in order (row t = position L - w + t)."""
         w = self.policy.window
-        return torch.roll(self.ring, shifts=-(self.count % w), dims=3).contiguous()
+        return torch.roll(self.ring, shifts=-(self.count % w), dims=0).permute(1, 2, 3, 0, 4).contiguous()
 
     def window_stats(self) -> torch.Tensor:
         """Decode statistics of the last w tokens in order, [NL][B][Hq][w][2]."""

@@ -345,7 +345,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the hot path is built and timed on a single MI355X "
-              "(see the sharding notes in DESIGN.md); run it with --gpus 1", file=sys.stderr)
+              "(units of (layer, sequence, KV head) would shard across GPUs with no exchange, but no "
+              "multi-GPU path is built); run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)

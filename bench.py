@@ -294,15 +294,17 @@ def cpu_baseline(w: Workload, comp_budget_s: float = 8.0, dec_budget_s: float = 
     NL, Bsz, H, Cap, D = w.shape
     scale = 1.0 / math.sqrt(D)
     r = [oracle.retention_from_reward(float(v)) for v in ci.reward]
+    cpu_s = 0.0                      # process CPU time (all threads) inside the timed oracle calls
     t_comp, n_comp = 0.0, 0
     comp = None
     while n_comp < NL and (n_comp == 0 or t_comp < comp_budget_s):
         Kl, Vl = I.to_f64(ci.k[n_comp])[None], I.to_f64(ci.v[n_comp])[None]
         Ql = I.to_f64(ci.q_win[n_comp])[None]
         lens = ci.length.numpy()[n_comp:n_comp + 1].astype(np.int64)
-        t0 = time.perf_counter()
+        c0, t0 = time.process_time(), time.perf_counter()
         res = oracle.compress_cache(Kl, Vl, lens, Ql, r, wl.window, scale)
         t_comp += time.perf_counter() - t0
+        cpu_s += time.process_time() - c0
         comp = comp or res
         n_comp += 1
     _, _, K2, V2, l2 = comp
@@ -316,14 +318,18 @@ def cpu_baseline(w: Workload, comp_budget_s: float = 8.0, dec_budget_s: float = 
         # the appended token); the sample attends over the same number of rows
         # without writing the appended row, so the cache needs no copy.
         lens_s = l2 + s_idx + 1
-        t0 = time.perf_counter()
+        c0, t0 = time.process_time(), time.perf_counter()
         oracle.decode_cache(K2, V2, lens_s, q1, scale)
         t_dec += time.perf_counter() - t0
+        cpu_s += time.process_time() - c0
         n_dec += 1
+    # Average number of busy host threads over the timed oracle calls.
+    busy = cpu_s / max(t_comp + t_dec, 1e-9)
     m_seq = l2[0, :, 0]
     comp_tok, dec_tok = kv_tokens(w, m_seq)
     est_step_s = NL * t_comp / n_comp + NL * wl.decode_steps * t_dec / n_dec
-    return {"value": (comp_tok + dec_tok) / est_step_s, "unit": "KV tokens/s", "cores": int(cores), "kind": "oracle",
+    return {"value": (comp_tok + dec_tok) / est_step_s, "unit": "KV tokens/s", "cores": int(cores),
+            "avg_busy_threads": round(busy, 2), "kind": "oracle",
             "sample": (f"{n_comp} of {NL} layers compressed ({n_comp * H * Bsz} units, {t_comp:.2f} s) and "
                        f"{n_dec} decode steps of 1 layer spread over the {wl.decode_steps}-step range "
                        f"({t_dec:.2f} s); per-phase rates scaled to one full step "

@@ -74,7 +74,10 @@ def test_trajectory_matches_oracle_replay(retention, dtype, variant):
     z_dev = logits.to(dev)
     bi, probes, fed = 0, [], []
     for tok in range(n_tokens):
-        out, lse = dec.decode(qs[tok].to(dev), ks[tok].to(dev), vs[tok].to(dev), logits=z_dev[tok])
+        q_dev = qs[tok].to(dev)
+        if tok % 2:
+            q_dev = dec.query_slot().copy_(q_dev)         # the caller writes the query into the ring itself
+        out, lse = dec.decode(q_dev, ks[tok].to(dev), vs[tok].to(dev), logits=z_dev[tok])
         ref, rl = oracle.decode_cache(K, V, lens, f64(qs[tok]), scale, f64(ks[tok]), f64(vs[tok]))
         assert_decode_close(out, ref, dtype, f"token {tok}")
         assert_lse_close(lse, rl, dtype, f"token {tok}")

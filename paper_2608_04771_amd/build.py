@@ -2,7 +2,8 @@
 
 Usage: ``python -m paper_2608_04771_amd.build`` or ``build_library()``.
 Always recompiles; the objects go to ``paper_2608_04771_amd/_build/`` and the
-library to ``paper_2608_04771_amd/libreco.so``."""
+library to ``paper_2608_04771_amd/libreco.so``.  ``build_c_driver()`` then
+compiles ``tests/c_abi/reco_c_driver``, a plain C client of the ABI."""
 from __future__ import annotations
 
 import concurrent.futures as cf
@@ -67,6 +68,27 @@ def build_library(verbose: bool = False) -> str:
     return LIB
 
 
+C_DRIVER_SRC = os.path.join(ROOT, "tests", "c_abi", "reco_c_driver.c")
+C_DRIVER = os.path.join(ROOT, "tests", "c_abi", "reco_c_driver")
+
+
+def build_c_driver() -> str:
+    """Compile the plain C11 client of the ABI (a GPU test runs it) against the
+    built libreco.so and the HIP runtime, with gcc: no HIP device code in it."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        raise RuntimeError("no C compiler found for the C ABI client")
+    tmp = C_DRIVER + ".tmp"
+    _run([cc, "-std=c11", "-O2", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+          f"-I{os.path.join(rocm, 'include')}", f"-I{os.path.join(ROOT, 'include')}", C_DRIVER_SRC, "-o", tmp,
+          f"-L{PKG}", "-lreco", f"-L{os.path.join(rocm, 'lib')}", "-lamdhip64",
+          "-Wl,-rpath,$ORIGIN/../../paper_2608_04771_amd", f"-Wl,-rpath,{os.path.join(rocm, 'lib')}"])
+    os.replace(tmp, C_DRIVER)
+    return C_DRIVER
+
+
 if __name__ == "__main__":
     path = build_library(verbose="-v" in sys.argv)
     print(path)
+    print(build_c_driver())

@@ -48,9 +48,9 @@ ANSWER_LEN = 32
 DECODE_TRAFFIC = {
     "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
                 "paper_2608_04771_amd/csrc/decode_attn.hpp"),
-    "sha256": "68181b4adbd35b5d0c85b322ae9f9aff2dd23d55ebe0fb639aaa91e008ee0b49",
+    "sha256": "c32943c7a959a935db735c184a74d62495d0a4c6a6f2b30369b0685d872f471f",
     "workload": "7b-28L-28q4kv-d128-bf16-L16384",
-    "fetch_bytes": 555425205,
+    "fetch_bytes": 555477303,
     "write_bytes": 817152,
 }
 

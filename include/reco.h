@@ -195,7 +195,10 @@ reco_status_t reco_pool_scores(const reco_kv_cache_t *cache, int32_t layer0, int
  *                  kept for the window rows, they let reco_score skip its
  *                  normaliser pass (empty: (-inf, 0))
  * An append with len == capacity is not performed (the token still takes part
- * in the attention) and sets RECO_DEV_APPEND_OVERFLOW. */
+ * in the attention) and sets RECO_DEV_APPEND_OVERFLOW.
+ * The work is split over the compute units of the current device, so the
+ * workspace size depends on that device: query it with the device current
+ * that the call will run on. */
 size_t reco_decode_attn_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers,
                                        int32_t n_q_heads);
 reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,

@@ -5,6 +5,8 @@
 
 #include <hip/hip_runtime.h>
 #include <math.h>
+
+#include <atomic>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -43,6 +45,21 @@ int group_of(const reco_kv_cache_t *c, int32_t n_q_heads) {
 }
 
 reco_status_t hip_status(hipError_t e) { return e == hipSuccess ? RECO_OK : RECO_ERR_HIP; }
+
+// Compute units of the current device, read once per device (256 on a whole
+// MI355X; a partitioned GPU shows fewer).  Falls back to 256 if the query
+// fails, which only changes the split count, never correctness.
+int current_compute_units() {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cached[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n > 0) return n;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) n = 256;
+  cached[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
 
 }  // namespace
 
@@ -222,7 +239,7 @@ reco_status_t reco_pool_scores(const reco_kv_cache_t *cache, int32_t layer0, int
 size_t reco_decode_attn_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers, int32_t n_q_heads) {
   if (!cache_ok(cache) || !units_ok(cache, n_layers) || group_of(cache, n_q_heads) < 1) return 0;
   const int units = n_layers * cache->batch * cache->n_kv_heads;
-  return reco::decode_workspace_bytes(units, cache->capacity, cache->head_dim);
+  return reco::decode_workspace_bytes(units, cache->capacity, cache->head_dim, current_compute_units());
 }
 
 reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers, const void *q,
@@ -239,7 +256,8 @@ reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int
   if (st != RECO_OK) return st;
   if (G > 16) return RECO_ERR_UNSUPPORTED;
   const int units = n_layers * cache->batch * cache->n_kv_heads;
-  const size_t need = reco::decode_workspace_bytes(units, cache->capacity, cache->head_dim);
+  const int cus = current_compute_units();
+  const size_t need = reco::decode_workspace_bytes(units, cache->capacity, cache->head_dim, cus);
   if (!ws || ws_bytes < need) return RECO_ERR_WORKSPACE;
 
   reco::DecodeParams p{};
@@ -252,7 +270,7 @@ reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int
   p.out = out;
   p.lse = lse;
   p.row_stats = row_stats;
-  p.splits = reco::decode_splits(units, cache->capacity);
+  p.splits = reco::decode_splits(units, cache->capacity, cus);
   p.part_o = reinterpret_cast<float *>(ws);
   p.part_ml = p.part_o + static_cast<size_t>(units) * p.splits * 16 * cache->head_dim;
   p.dev_err = dev_err;

@@ -601,13 +601,13 @@ hipError_t launch_typed(const DecodeParams &p, hipStream_t s) {
 
 }  // namespace
 
-// Splits per unit: at most one workgroup per compute unit (MI355X has 256).
-// Measured on the 7B-shaped cache, a single resident round with one
-// workgroup per CU streams fastest: two workgroups sharing a CU finish later
-// than the rest, and a second round adds its ramp to the tail.  At least
-// four 32-key tiles per split at capacity.
-int decode_splits(int units, int capacity) {
-  const int compute_units = 256;
+// Splits per unit: at most one workgroup per compute unit of the device
+// (256 on a whole MI355X, fewer on a partition of it).  Measured on the
+// 7B-shaped cache, a single resident round with one workgroup per CU streams
+// fastest: two workgroups sharing a CU finish later than the rest, and a
+// second round adds its ramp to the tail.  At least four 32-key tiles per
+// split at capacity.
+int decode_splits(int units, int capacity, int compute_units) {
   const int tiles_cap = (capacity + 1 + kTile - 1) / kTile;
   int splits = compute_units / units;
   int max_splits = tiles_cap / 4;
@@ -618,8 +618,8 @@ int decode_splits(int units, int capacity) {
   return splits;
 }
 
-size_t decode_workspace_bytes(int units, int capacity, int head_dim) {
-  const size_t splits = static_cast<size_t>(decode_splits(units, capacity));
+size_t decode_workspace_bytes(int units, int capacity, int head_dim, int compute_units) {
+  const size_t splits = static_cast<size_t>(decode_splits(units, capacity, compute_units));
   return static_cast<size_t>(units) * splits * (16 * static_cast<size_t>(head_dim) + 32) * sizeof(float);
 }
 

@@ -25,8 +25,9 @@ struct DecodeParams {
   int layer0, n_layers, batch, hkv, cap, group, hq, splits;
   float scale_log2;       // logit scale * log2(e)
 };
-int decode_splits(int units, int capacity);
-size_t decode_workspace_bytes(int units, int capacity, int head_dim);
+// compute_units: CUs of the device the call runs on (sets the split count).
+int decode_splits(int units, int capacity, int compute_units);
+size_t decode_workspace_bytes(int units, int capacity, int head_dim, int compute_units);
 hipError_t launch_decode(const DecodeParams &p, int dtype, int head_dim, hipStream_t s);
 
 }  // namespace reco

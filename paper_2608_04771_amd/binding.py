@@ -113,12 +113,24 @@ def _check(status: int, what: str):
 
 
 def _need_cuda(*ts):
+    """Every given tensor (None skipped) is a contiguous tensor on one GPU."""
+    dev = None
     for t in ts:
         if t is not None:
             if not t.is_cuda:
                 raise ValueError("tensors must live on the GPU")
             if not t.is_contiguous():
                 raise ValueError("tensors must be contiguous")
+            d = t.get_device()
+            if dev is None:
+                dev = d
+            elif d != dev:
+                raise ValueError("tensors of one call must live on the same GPU")
+
+
+def _same_gpu(a: torch.Tensor, b: torch.Tensor):
+    if not a.is_cuda or a.get_device() != b.get_device():
+        raise ValueError("tensors of one call must live on the same GPU")
 
 
 class KVCache:
@@ -205,7 +217,7 @@ def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[floa
         scores = torch.zeros((nl, B, H, Cap), dtype=torch.float32, device=cache.k.device)
     if row_stats is not None and (row_stats.dtype != torch.float32 or tuple(row_stats.shape) != (nl, B, hq, w, 2)):
         raise ValueError("row_stats must be float32 [n_layers][B][Hq][w][2]")
-    _need_cuda(q_win, scores, ws, dev_err, row_stats)
+    _need_cuda(cache.k, q_win, scores, ws, dev_err, row_stats)
     ws = _ws(lambda: score_workspace_size(cache, hq, w, nl), cache.k.device, ws)
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     st = load_library().reco_score(cache.ref(), layer0, nl, _ptr(q_win), hq, w, scale,
@@ -236,7 +248,7 @@ def reco_select_compact(cache: KVCache, scores: torch.Tensor, retention: torch.T
         raise ValueError("scores must be float32")
     if kept_idx is not None and kept_idx.dtype != torch.int32:
         raise ValueError("kept_idx must be int32")
-    _need_cuda(scores, retention, kept_idx, ws, dev_err)
+    _need_cuda(cache.k, scores, retention, kept_idx, ws, dev_err)
     ws = _ws(lambda: select_compact_workspace_size(cache, nl), cache.k.device, ws)
     st = load_library().reco_select_compact(cache.ref(), layer0, nl, _ptr(scores), _ptr(retention), stride, w,
                                             _ptr(kept_idx), _ptr(ws), ws.numel(), _ptr(dev_err),
@@ -257,7 +269,7 @@ def reco_pool_scores(cache: KVCache, scores: torch.Tensor, w: int, kernel: int, 
         raise ValueError("mode must be 'max' or 'mean'")
     if pooled is None:
         pooled = torch.zeros_like(scores)
-    _need_cuda(scores, pooled, dev_err)
+    _need_cuda(cache.k, scores, pooled, dev_err)
     st = load_library().reco_pool_scores(cache.ref(), layer0, nl, w, _ptr(scores), _ptr(pooled), kernel,
                                          RECO_POOL_MAX if mode == "max" else RECO_POOL_MEAN, _ptr(dev_err),
                                          _stream(cache.k.device))
@@ -284,7 +296,7 @@ def reco_decode_attn(cache: KVCache, q: torch.Tensor, k_new: Optional[torch.Tens
         lse = torch.empty((nl, B, hq), dtype=torch.float32, device=q.device)
     if row_stats is not None and (row_stats.dtype != torch.float32 or tuple(row_stats.shape) != (nl, B, hq, 2)):
         raise ValueError("row_stats must be float32 [n_layers][B][Hq][2]")
-    _need_cuda(q, k_new, v_new, out, lse, ws, dev_err, row_stats)
+    _need_cuda(cache.k, q, k_new, v_new, out, lse, ws, dev_err, row_stats)
     ws = _ws(lambda: decode_attn_workspace_size(cache, hq, nl), q.device, ws)
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     st = load_library().reco_decode_attn(cache.ref(), layer0, nl, _ptr(q), hq, scale, _ptr(k_new), _ptr(v_new),
@@ -302,10 +314,8 @@ def reco_logit_penalty(logits: torch.Tensor, refl_ids: torch.Tensor, reward: tor
         raise ValueError("logits must be fp32 [rows][vocab] with unit column stride")
     if refl_ids.dtype != torch.int32 or reward.dtype != torch.float32:
         raise ValueError("refl_ids int32, reward float32")
-    for t in (refl_ids, reward, dev_err):
-        _need_cuda(t)
-    if not logits.is_cuda:
-        raise ValueError("logits must live on the GPU")
+    _need_cuda(refl_ids, reward, dev_err)
+    _same_gpu(logits, reward)
     rows, vocab = logits.shape
     st = load_library().reco_logit_penalty(_ptr(logits), rows, vocab, logits.stride(0), _ptr(refl_ids),
                                            refl_ids.numel(), _ptr(reward), tau_lo, tau_hi, beta_lo, beta_mid,
@@ -324,14 +334,13 @@ def reco_penalty_sample(logits: torch.Tensor, refl_ids: Optional[torch.Tensor], 
         raise ValueError("logits must be fp32 [rows][vocab] with unit column stride")
     if (refl_ids is not None and refl_ids.dtype != torch.int32) or reward.dtype != torch.float32:
         raise ValueError("refl_ids int32, reward float32")
-    if not logits.is_cuda:
-        raise ValueError("logits must live on the GPU")
     rows, vocab = logits.shape
-    if tokens is None:
+    if tokens is None and logits.is_cuda:
         tokens = torch.empty(rows, dtype=torch.int32, device=logits.device)
-    if tokens.dtype != torch.int32:
+    if tokens is not None and tokens.dtype != torch.int32:
         raise ValueError("tokens must be int32")
-    _need_cuda(refl_ids, reward, tokens, ws, dev_err)
+    _need_cuda(reward, refl_ids, tokens, ws, dev_err)
+    _same_gpu(logits, reward)
     ws = _ws(lambda: penalty_sample_workspace_size(rows, vocab), logits.device, ws)
     n_refl = 0 if refl_ids is None else refl_ids.numel()
     st = load_library().reco_penalty_sample(_ptr(logits), rows, vocab, logits.stride(0), _ptr(refl_ids), n_refl,

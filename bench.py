@@ -433,6 +433,8 @@ def main():
         "pct_of_peak_hbm": 100.0 * step_bytes / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS,
         "algorithmic_bytes_per_step": step_bytes,
         "kv_tokens_per_step": {"compress": comp_tok, "decode": dec_tok},
+        "compress_algorithmic_bytes": {"score": ab["score"], "select": ab["select"], "compact": ab["compact"],
+                                       "compact_moved_rows": moved},
         "phase_ms": {"score": float(score_ms.mean()), "select_compact": float(sel_ms.mean()),
                      "compress": float(comp_ms.mean()), "decode_call": dec_avg_ms,
                      "decode_calls_total": float(dec_loop_ms.mean()), "answer_ppl": float(ppl_ms.mean())},

@@ -197,3 +197,18 @@ def test_decode_bad_length_is_reported(cap):
     kc, vc = cache.k.cpu(), cache.v.cpu()
     assert torch.equal(kc[0, 0, :2], k[0, 0, :2]) and torch.equal(vc[0, 0, :2], v[0, 0, :2])   # no append
     assert torch.equal(kc[0, 0, 2, 20], kn[0, 0, 2]) and torch.equal(vc[0, 0, 2, 20], vn[0, 0, 2])
+
+
+@pytest.mark.parametrize("units,cap", [(1, 20000), (4, 16640), (112, 16640), (256, 4096), (300, 4096), (4, 100)])
+def test_decode_workspace_follows_the_device_compute_units(units, cap):
+    """The split count is min(CUs / units, 128, capacity tiles / 4), at least
+    1, with the CU count read from the device: the workspace holds one
+    partial of 16 x D fp32 + 32 statistics per (unit, split)."""
+    D = 128
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    k = torch.zeros((1, 1, units, cap, D), dtype=torch.bfloat16, device="cuda")
+    ln = torch.zeros((1, 1, units), dtype=torch.int32, device="cuda")
+    cache = B.KVCache(k, k, ln)
+    tiles_cap = (cap + 1 + 31) // 32
+    splits = max(1, min(cus // units, 128, max(1, tiles_cap // 4)))
+    assert B.decode_attn_workspace_size(cache, units * 4) == units * splits * (16 * D + 32) * 4

@@ -122,7 +122,8 @@ typedef struct reco_kv_cache {
  *           decoded (the keys it saw then are keys 0..p now), with the same
  *           scale; requires RECO_SCORE_CAUSAL.
  *   scores: [n_layers][batch][n_kv_heads][capacity] fp32 (output)
- * Requires 1 <= w <= capacity and G * w <= 4096.  Accumulation is fp32. */
+ * Requires 1 <= w <= capacity, G * w <= 4096 and capacity <= 2^29 (larger:
+ * RECO_ERR_UNSUPPORTED).  Accumulation is fp32. */
 size_t reco_score_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers,
                                  int32_t n_q_heads, int32_t w);
 reco_status_t reco_score(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,

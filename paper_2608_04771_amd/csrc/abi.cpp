@@ -18,6 +18,10 @@ namespace {
 // length) and row offsets then stay far inside int32.
 constexpr int32_t kMaxVocab = 1 << 30;
 
+// Largest capacity the score kernels take: their grid spans 8 x chunks
+// workgroups of 256 threads along x, which must stay below 2^32 work-items.
+constexpr int32_t kMaxScoreCapacity = 1 << 29;
+
 bool cache_ok(const reco_kv_cache_t *c) {
   return c && c->k && c->v && c->len && c->n_layers >= 1 && c->batch >= 1 && c->n_kv_heads >= 1 &&
          c->capacity >= 1;
@@ -119,7 +123,7 @@ int32_t reco_kept_count(int32_t L, int32_t w, double r) {
 
 // ---------------------------------------------------------------- score
 size_t reco_score_workspace_size(const reco_kv_cache_t *cache, int32_t n_layers, int32_t n_q_heads, int32_t w) {
-  if (!cache_ok(cache) || !units_ok(cache, n_layers) || w < 1) return 0;
+  if (!cache_ok(cache) || !units_ok(cache, n_layers) || w < 1 || cache->capacity > kMaxScoreCapacity) return 0;
   const int G = group_of(cache, n_q_heads);
   if (G < 1 || static_cast<int64_t>(G) * w > reco::kScoreMaxRows) return 0;
   const int units = n_layers * cache->batch * cache->n_kv_heads;
@@ -138,6 +142,7 @@ reco_status_t reco_score(const reco_kv_cache_t *cache, int32_t layer0, int32_t n
   reco_status_t st = cache_supported(cache);
   if (st != RECO_OK) return st;
   if (static_cast<int64_t>(G) * w > reco::kScoreMaxRows) return RECO_ERR_UNSUPPORTED;
+  if (cache->capacity > kMaxScoreCapacity) return RECO_ERR_UNSUPPORTED;
   const size_t need = reco_score_workspace_size(cache, n_layers, n_q_heads, w);
   if (!ws || ws_bytes < need) return RECO_ERR_WORKSPACE;
 

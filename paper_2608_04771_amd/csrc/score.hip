@@ -65,6 +65,20 @@ __device__ __forceinline__ UnitInfo unit_info(const ScoreParams &p, int unit) {
   return u;
 }
 
+// Workgroup -> (chunk, unit) for the statistics and mass passes.  The
+// dispatcher hands consecutive workgroup ids to the eight XCDs in turn, and
+// every XCD has its own L2; ids are laid out so that all chunks of a unit
+// share one id residue mod 8 (one XCD), so each unit's window queries, which
+// every chunk of the unit reads, come from HBM once instead of once per XCD.
+// The grid is (8 x chunks, units / 8 rounded up): workgroup (x, y) has id
+// y * 8 * chunks + x, so id mod 8 = x mod 8; it takes unit 8y + x mod 8 and
+// chunk x / 8.  Padding workgroups (unit past the last) return at once.
+__device__ __forceinline__ bool xcd_chunk_unit(const ScoreParams &p, int &chunk, int &unit) {
+  unit = static_cast<int>(blockIdx.y) * 8 + static_cast<int>(blockIdx.x & 7);
+  chunk = static_cast<int>(blockIdx.x >> 3);
+  return unit < p.n_layers * p.batch * p.hkv;
+}
+
 template <typename T, int D>
 struct ScoreCfg {
   using MF = Mfma<T>;
@@ -229,8 +243,9 @@ __global__ __launch_bounds__(kThreads, 2) void score_stats_kernel(ScoreParams p)
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int col = lane & 15, grp = lane >> 4;
-  const int chunk = blockIdx.x;
-  const UnitInfo u = unit_info(p, blockIdx.y);
+  int chunk, unit;
+  if (!xcd_chunk_unit(p, chunk, unit)) return;
+  const UnitInfo u = unit_info(p, unit);
   const int k0 = chunk * kScoreChunk;
   if (k0 >= u.L) return;
   const int k1 = min(u.L, k0 + kScoreChunk);
@@ -336,8 +351,9 @@ __global__ __launch_bounds__(kThreads, 2) void score_mass_kernel(ScoreParams p) 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int col = lane & 15, grp = lane >> 4;
-  const int chunk = blockIdx.x;
-  const UnitInfo u = unit_info(p, blockIdx.y);
+  int chunk, unit;
+  if (!xcd_chunk_unit(p, chunk, unit)) return;
+  const UnitInfo u = unit_info(p, unit);
   const int k0 = chunk * kScoreChunk;
   if (k0 >= u.L) return;
   const int k1 = min(u.L, k0 + kScoreChunk);
@@ -450,7 +466,8 @@ hipError_t launch_rtw(const ScoreParams &p, int waves, hipStream_t s) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   } else {
-    hipLaunchKernelGGL((score_stats_kernel<T, D, RTW>), dim3(p.chunks, units), dim3(waves * kWave), 0, s, p);
+    hipLaunchKernelGGL((score_stats_kernel<T, D, RTW>), dim3(8 * p.chunks, (units + 7) / 8), dim3(waves * kWave), 0, s,
+                       p);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(score_rowmerge_kernel, dim3((p.rows_pad + kThreads - 1) / kThreads, units), dim3(kThreads), 0,
@@ -458,7 +475,8 @@ hipError_t launch_rtw(const ScoreParams &p, int waves, hipStream_t s) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((score_mass_kernel<T, D, RTW>), dim3(p.chunks, units), dim3(waves * kWave), 0, s, p);
+  hipLaunchKernelGGL((score_mass_kernel<T, D, RTW>), dim3(8 * p.chunks, (units + 7) / 8), dim3(waves * kWave), 0, s,
+                     p);
   return hipGetLastError();
 }
 

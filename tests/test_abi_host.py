@@ -98,6 +98,7 @@ def test_score_rejects_bad_arguments():
     assert _score(ok, wsb=16) == B.RECO_ERR_WORKSPACE
     big = _fake_cache(capacity=100000)
     assert _score(big, hq=2 * 100, w=100) == B.RECO_ERR_UNSUPPORTED      # G*w = 10000 rows > 4096
+    assert _score(_fake_cache(capacity=(1 << 29) + 1)) == B.RECO_ERR_UNSUPPORTED   # beyond the score grid
 
 
 def test_select_compact_rejects_bad_arguments():
@@ -230,7 +231,7 @@ def test_workspace_sizes_are_positive_and_monotone():
 def test_workspace_sizes_reject_shapes_the_calls_reject():
     """Sizes are 0 (never an overflowed number) for shapes the entry points
     refuse: too many units for one grid dimension, G * w beyond the score's
-    row limit, a vocabulary beyond 2^30."""
+    row limit, a score capacity beyond 2^29, a vocabulary beyond 2^30."""
     lib = B.load_library()
     many = _fake_cache(batch=40000, n_kv_heads=2)                        # 80,000 units per layer
     assert lib.reco_score_workspace_size(ctypes.byref(many), 1, 2, 8) == 0
@@ -240,6 +241,8 @@ def test_workspace_sizes_reject_shapes_the_calls_reject():
     assert lib.reco_score_workspace_size(ctypes.byref(ok), 2, 2 * 64, 64) > 0      # G*w = 4096, the limit
     assert lib.reco_score_workspace_size(ctypes.byref(ok), 2, 2 * 65, 64) == 0     # 4160 rows
     assert lib.reco_score_workspace_size(ctypes.byref(ok), 2, 2, 2 ** 31 - 1) == 0
+    huge = _fake_cache(capacity=(1 << 29) + 1)                          # beyond the score grid's reach
+    assert lib.reco_score_workspace_size(ctypes.byref(huge), 1, 2, 8) == 0
     assert lib.reco_penalty_sample_workspace_size(3, 1 << 30) >= 3 * (1 << 20) * 8
     assert lib.reco_penalty_sample_workspace_size(3, 2 ** 31 - 1) == 0
     assert lib.reco_answer_ppl_workspace_size(1, 1, 2 ** 31 - 1) == 0

@@ -227,10 +227,18 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
 template <int ROWB>
 __global__ __launch_bounds__(kCompThreads) void compact_kernel(SelectParams p) {
   constexpr int kSlices = ROWB / kSliceBytes;
-  const int wg = blockIdx.x;
-  const int slice = wg % kSlices;
-  const int tensor = (wg / kSlices) % 2;
-  const int unit = wg / (kSlices * 2);
+  constexpr int kPerUnit = 2 * kSlices;             // (K or V) x slice workgroups of one unit
+  // XCD-aware order: consecutive workgroup ids go to the eight XCDs in turn,
+  // so ids are laid out in groups of 8 units x kPerUnit with every workgroup
+  // of a unit at the same id mod 8: they share one XCD's L2 and the unit's
+  // kept list is fetched from HBM once.  Padding workgroups return at once.
+  const int grp8 = static_cast<int>(blockIdx.x) / (8 * kPerUnit);
+  const int r8 = static_cast<int>(blockIdx.x) - grp8 * 8 * kPerUnit;
+  const int unit = grp8 * 8 + (r8 & 7);
+  const int job = r8 >> 3;
+  const int slice = job % kSlices;
+  const int tensor = job / kSlices;
+  if (unit >= p.n_layers * p.batch * p.hkv) return;
   const int per_layer = p.batch * p.hkv;
   const int lc = unit / per_layer;
   const int b = (unit % per_layer) / p.hkv;
@@ -291,13 +299,13 @@ hipError_t launch_select_compact(const SelectParams &p, int dtype, int head_dim,
   const int rowb = head_dim * (dtype == 0 ? 4 : 2);
   switch (rowb) {
     case 128:
-      hipLaunchKernelGGL(compact_kernel<128>, dim3(units * 2 * 1), dim3(kCompThreads), 0, s, p);
+      hipLaunchKernelGGL(compact_kernel<128>, dim3((units + 7) / 8 * 8 * 2 * 1), dim3(kCompThreads), 0, s, p);
       break;
     case 256:
-      hipLaunchKernelGGL(compact_kernel<256>, dim3(units * 2 * 2), dim3(kCompThreads), 0, s, p);
+      hipLaunchKernelGGL(compact_kernel<256>, dim3((units + 7) / 8 * 8 * 2 * 2), dim3(kCompThreads), 0, s, p);
       break;
     default:
-      hipLaunchKernelGGL(compact_kernel<512>, dim3(units * 2 * 4), dim3(kCompThreads), 0, s, p);
+      hipLaunchKernelGGL(compact_kernel<512>, dim3((units + 7) / 8 * 8 * 2 * 4), dim3(kCompThreads), 0, s, p);
       break;
   }
   return hipGetLastError();

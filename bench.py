@@ -284,11 +284,22 @@ def cpu_baseline(w: Workload, comp_budget_s: float = 8.0, dec_budget_s: float = 
     layer spread over the decode range, until each phase has used its time
     budget; the per-phase rates are then scaled to one full step."""
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
+    # Host cores this process may run on; the oracle's BLAS pool is set to
+    # that count, capped by the job's thread budget (OMP_NUM_THREADS) where
+    # one is set, so that it never oversubscribes the cores it was given.
+    affinity = len(os.sched_getaffinity(0))
+    budget = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    threads = min(affinity, budget) if budget > 0 else affinity
+    with threadpool_limits(limits=threads):
         cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    except Exception:  # pragma: no cover
-        cores = 1
+        res = _cpu_baseline_sample(w, oracle, comp_budget_s, dec_budget_s)
+    res["cores"] = int(cores)
+    res["affinity_cores"] = affinity
+    return res
+
+
+def _cpu_baseline_sample(w: Workload, oracle, comp_budget_s: float, dec_budget_s: float):
     wl = w.wl
     ci = w.ci
     NL, Bsz, H, Cap, D = w.shape
@@ -328,7 +339,7 @@ def cpu_baseline(w: Workload, comp_budget_s: float = 8.0, dec_budget_s: float = 
     m_seq = l2[0, :, 0]
     comp_tok, dec_tok = kv_tokens(w, m_seq)
     est_step_s = NL * t_comp / n_comp + NL * wl.decode_steps * t_dec / n_dec
-    return {"value": (comp_tok + dec_tok) / est_step_s, "unit": "KV tokens/s", "cores": int(cores),
+    return {"value": (comp_tok + dec_tok) / est_step_s, "unit": "KV tokens/s",
             "avg_busy_threads": round(busy, 2), "kind": "oracle",
             "sample": (f"{n_comp} of {NL} layers compressed ({n_comp * H * Bsz} units, {t_comp:.2f} s) and "
                        f"{n_dec} decode steps of 1 layer spread over the {wl.decode_steps}-step range "

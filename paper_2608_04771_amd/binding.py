@@ -133,18 +133,42 @@ def _same_gpu(a: torch.Tensor, b: torch.Tensor):
         raise ValueError("tensors of one call must live on the same GPU")
 
 
+_DT = {torch.float32: "float32", torch.bfloat16: "bfloat16", torch.float64: "float64", torch.int32: "int32",
+       torch.uint8: "uint8"}
+
+
+def _expect(t: Optional[torch.Tensor], what: str, shape, dtype: torch.dtype):
+    """The C ABI sees only pointers, so every tensor it indexes is checked here
+    against the exact shape and dtype the call reads or writes: an undersized
+    or mistyped buffer would otherwise be read or written out of bounds."""
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype:
+        raise ValueError(f"{what} must be {_DT.get(dtype, dtype)} {list(shape)}, "
+                         f"got {_DT.get(t.dtype, t.dtype)} {list(t.shape)}")
+
+
+def _expect_dev_err(dev_err: Optional[torch.Tensor]):
+    if dev_err is not None and (dev_err.dtype != torch.int32 or dev_err.numel() < 1):
+        raise ValueError("dev_err must be an int32 tensor with at least one element")
+
+
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
 class KVCache:
     """A KV cache in the library's layout: K and V ``[NL][B][H][Cap][D]``
     (fp32 or bf16), ``length`` ``[NL][B][H]`` int32, all on the GPU."""
 
     def __init__(self, k: torch.Tensor, v: torch.Tensor, length: torch.Tensor):
-        _need_cuda(k, v, length)
         if k.shape != v.shape or k.dim() != 5 or k.dtype != v.dtype:
             raise ValueError("k and v must share a [NL][B][H][Cap][D] shape and dtype")
         if k.dtype not in (torch.float32, torch.bfloat16):
             raise ValueError("cache dtype must be float32 or bfloat16")
         if length.dtype != torch.int32 or tuple(length.shape) != tuple(k.shape[:3]):
             raise ValueError("length must be int32 [NL][B][H]")
+        _need_cuda(k, v, length)
         self.k, self.v, self.length = k, v, length
         NL, B, H, Cap, D = k.shape
         self.struct = RecoKVCache(k.data_ptr(), v.data_ptr(), length.data_ptr(), NL, B, H, Cap, D,
@@ -159,7 +183,11 @@ class KVCache:
 
 
 def _layers(cache: KVCache, layer0: int, n_layers: Optional[int]):
-    return layer0, (cache.shape[0] - layer0) if n_layers is None else n_layers
+    layer0 = int(layer0)
+    nl = (cache.shape[0] - layer0) if n_layers is None else int(n_layers)
+    if layer0 < 0 or nl < 1 or layer0 + nl > cache.shape[0]:
+        raise ValueError(f"layers [{layer0}, {layer0 + nl}) outside the cache's {cache.shape[0]} layers")
+    return layer0, nl
 
 
 def score_workspace_size(cache: KVCache, n_q_heads: int, w: int, n_layers: Optional[int] = None) -> int:
@@ -199,33 +227,54 @@ def decode_workspace(cache: "KVCache", n_q_heads: int, n_layers: Optional[int] =
     return _ws(lambda: decode_attn_workspace_size(cache, n_q_heads, n_layers), cache.k.device, None)
 
 
-def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[float] = None, causal: bool = True,
-               scores: Optional[torch.Tensor] = None, layer0: int = 0, n_layers: Optional[int] = None,
-               ws: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None,
-               row_stats: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Eq. 2 window attention mass; returns scores [NL][B][H][Cap] fp32.
-    ``row_stats`` ([n_layers][B][Hq][w][2], from the window tokens' decode
-    steps) replaces the normaliser pass over K."""
-    layer0, nl = _layers(cache, layer0, n_layers)
+def _score_shapes(cache: KVCache, nl: int, q_win: torch.Tensor, w: int, scores, row_stats):
     NL, B, H, Cap, D = cache.shape
     if q_win.dim() != 5 or q_win.shape[0] != nl or q_win.shape[1] != B or q_win.shape[3] != w or q_win.shape[4] != D:
         raise ValueError("q_win must be [n_layers][B][Hq][w][D]")
     if q_win.dtype != cache.k.dtype:
         raise ValueError("q_win must have the cache dtype")
     hq = q_win.shape[2]
+    _expect(scores, "scores", (nl, B, H, Cap), torch.float32)
+    _expect(row_stats, "row_stats", (nl, B, hq, w, 2), torch.float32)
+    return hq
+
+
+def reco_score(cache: KVCache, q_win: torch.Tensor, w: int, scale: Optional[float] = None, causal: bool = True,
+               scores: Optional[torch.Tensor] = None, layer0: int = 0, n_layers: Optional[int] = None,
+               ws: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None,
+               row_stats: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Eq. 2 window attention mass; returns scores [n_layers][B][H][Cap] fp32.
+    ``row_stats`` ([n_layers][B][Hq][w][2], from the window tokens' decode
+    steps) replaces the normaliser pass over K."""
+    layer0, nl = _layers(cache, layer0, n_layers)
+    hq = _score_shapes(cache, nl, q_win, w, scores, row_stats)
+    _expect_dev_err(dev_err)
+    NL, B, H, Cap, D = cache.shape
+    _need_cuda(cache.k, q_win, scores, ws, dev_err, row_stats)
     if scores is None:
         scores = torch.zeros((nl, B, H, Cap), dtype=torch.float32, device=cache.k.device)
-    if row_stats is not None and (row_stats.dtype != torch.float32 or tuple(row_stats.shape) != (nl, B, hq, w, 2)):
-        raise ValueError("row_stats must be float32 [n_layers][B][Hq][w][2]")
-    _need_cuda(cache.k, q_win, scores, ws, dev_err, row_stats)
     ws = _ws(lambda: score_workspace_size(cache, hq, w, nl), cache.k.device, ws)
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     st = load_library().reco_score(cache.ref(), layer0, nl, _ptr(q_win), hq, w, scale,
                                    RECO_SCORE_CAUSAL if causal else 0, _ptr(row_stats), _ptr(scores), _ptr(ws),
-                                   ws.numel(),
-                                   _ptr(dev_err), _stream(cache.k.device))
+                                   _nbytes(ws), _ptr(dev_err), _stream(cache.k.device))
     _check(st, "reco_score")
     return scores
+
+
+def _select_shapes(cache: KVCache, nl: int, scores: torch.Tensor, retention: torch.Tensor, kept_idx):
+    NL, Bsz, H, Cap, D = cache.shape
+    if retention.dtype != torch.float64:
+        raise ValueError("retention must be float64")
+    if tuple(retention.shape) == (Bsz,):
+        stride = 0
+    elif tuple(retention.shape) == (nl, Bsz):
+        stride = Bsz
+    else:
+        raise ValueError("retention must be [B] or [n_layers][B]")
+    _expect(scores, "scores", (nl, Bsz, H, Cap), torch.float32)
+    _expect(kept_idx, "kept_idx", (nl, Bsz, H, Cap), torch.int32)
+    return stride
 
 
 def reco_select_compact(cache: KVCache, scores: torch.Tensor, retention: torch.Tensor, w: int,
@@ -235,23 +284,12 @@ def reco_select_compact(cache: KVCache, scores: torch.Tensor, retention: torch.T
     ``retention`` is float64 [B] (one level per sequence) or [n_layers][B]
     (per-layer budgets)."""
     layer0, nl = _layers(cache, layer0, n_layers)
-    Bsz = cache.shape[1]
-    if retention.dtype != torch.float64:
-        raise ValueError("retention must be float64")
-    if tuple(retention.shape) == (Bsz,):
-        stride = 0
-    elif tuple(retention.shape) == (nl, Bsz):
-        stride = Bsz
-    else:
-        raise ValueError("retention must be [B] or [n_layers][B]")
-    if scores.dtype != torch.float32:
-        raise ValueError("scores must be float32")
-    if kept_idx is not None and kept_idx.dtype != torch.int32:
-        raise ValueError("kept_idx must be int32")
+    stride = _select_shapes(cache, nl, scores, retention, kept_idx)
+    _expect_dev_err(dev_err)
     _need_cuda(cache.k, scores, retention, kept_idx, ws, dev_err)
     ws = _ws(lambda: select_compact_workspace_size(cache, nl), cache.k.device, ws)
     st = load_library().reco_select_compact(cache.ref(), layer0, nl, _ptr(scores), _ptr(retention), stride, w,
-                                            _ptr(kept_idx), _ptr(ws), ws.numel(), _ptr(dev_err),
+                                            _ptr(kept_idx), _ptr(ws), _nbytes(ws), _ptr(dev_err),
                                             _stream(cache.k.device))
     _check(st, "reco_select_compact")
     return kept_idx
@@ -263,18 +301,35 @@ def reco_pool_scores(cache: KVCache, scores: torch.Tensor, w: int, kernel: int, 
     """Max / mean pooling of the prefix scores (window scores copied); returns
     pooled [n_layers][B][H][Cap] fp32 (entries at or beyond len unwritten)."""
     layer0, nl = _layers(cache, layer0, n_layers)
-    if scores.dtype != torch.float32:
-        raise ValueError("scores must be float32")
+    NL, Bsz, H, Cap, D = cache.shape
     if mode not in ("max", "mean"):
         raise ValueError("mode must be 'max' or 'mean'")
+    _expect(scores, "scores", (nl, Bsz, H, Cap), torch.float32)
+    _expect(pooled, "pooled", (nl, Bsz, H, Cap), torch.float32)
+    _expect_dev_err(dev_err)
+    _need_cuda(cache.k, scores, pooled, dev_err)
     if pooled is None:
         pooled = torch.zeros_like(scores)
-    _need_cuda(cache.k, scores, pooled, dev_err)
     st = load_library().reco_pool_scores(cache.ref(), layer0, nl, w, _ptr(scores), _ptr(pooled), kernel,
                                          RECO_POOL_MAX if mode == "max" else RECO_POOL_MEAN, _ptr(dev_err),
                                          _stream(cache.k.device))
     _check(st, "reco_pool_scores")
     return pooled
+
+
+def _decode_shapes(cache: KVCache, nl: int, q: torch.Tensor, k_new, v_new, out, lse, row_stats):
+    NL, B, H, Cap, D = cache.shape
+    if q.dim() != 4 or q.shape[0] != nl or q.shape[1] != B or q.shape[3] != D or q.dtype != cache.k.dtype:
+        raise ValueError("q must be [n_layers][B][Hq][D] in the cache dtype")
+    hq = q.shape[2]
+    if (k_new is None) != (v_new is None):
+        raise ValueError("k_new and v_new must be given together")
+    _expect(k_new, "k_new", (nl, B, H, D), cache.k.dtype)
+    _expect(v_new, "v_new", (nl, B, H, D), cache.k.dtype)
+    _expect(out, "out", (nl, B, hq, D), cache.k.dtype)
+    _expect(lse, "lse", (nl, B, hq), torch.float32)
+    _expect(row_stats, "row_stats", (nl, B, hq, 2), torch.float32)
+    return hq
 
 
 def reco_decode_attn(cache: KVCache, q: torch.Tensor, k_new: Optional[torch.Tensor] = None,
@@ -286,37 +341,41 @@ def reco_decode_attn(cache: KVCache, q: torch.Tensor, k_new: Optional[torch.Tens
     ``row_stats`` ([n_layers][B][Hq][2] fp32) optionally receives each query's
     (max, sum) of the log2-domain logits."""
     layer0, nl = _layers(cache, layer0, n_layers)
+    hq = _decode_shapes(cache, nl, q, k_new, v_new, out, lse, row_stats)
+    _expect_dev_err(dev_err)
+    _need_cuda(cache.k, q, k_new, v_new, out, lse, ws, dev_err, row_stats)
     NL, B, H, Cap, D = cache.shape
-    if q.dim() != 4 or q.shape[0] != nl or q.shape[1] != B or q.shape[3] != D or q.dtype != cache.k.dtype:
-        raise ValueError("q must be [n_layers][B][Hq][D] in the cache dtype")
-    hq = q.shape[2]
     if out is None:
         out = torch.empty_like(q)
     if lse is None and want_lse:
         lse = torch.empty((nl, B, hq), dtype=torch.float32, device=q.device)
-    if row_stats is not None and (row_stats.dtype != torch.float32 or tuple(row_stats.shape) != (nl, B, hq, 2)):
-        raise ValueError("row_stats must be float32 [n_layers][B][Hq][2]")
-    _need_cuda(cache.k, q, k_new, v_new, out, lse, ws, dev_err, row_stats)
     ws = _ws(lambda: decode_attn_workspace_size(cache, hq, nl), q.device, ws)
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     st = load_library().reco_decode_attn(cache.ref(), layer0, nl, _ptr(q), hq, scale, _ptr(k_new), _ptr(v_new),
-                                         _ptr(out), _ptr(lse), _ptr(row_stats), _ptr(ws), ws.numel(), _ptr(dev_err),
-                                         _stream(q.device))
+                                         _ptr(out), _ptr(lse), _ptr(row_stats), _ptr(ws), _nbytes(ws),
+                                         _ptr(dev_err), _stream(q.device))
     _check(st, "reco_decode_attn")
     return out, lse
+
+
+def _logit_rows(logits: torch.Tensor):
+    if logits.dtype != torch.float32 or logits.dim() != 2 or logits.stride(1) != 1 or \
+            logits.stride(0) < logits.shape[1]:
+        raise ValueError("logits must be fp32 [rows][vocab] with unit column stride and row stride >= vocab")
+    return logits.shape
 
 
 def reco_logit_penalty(logits: torch.Tensor, refl_ids: torch.Tensor, reward: torch.Tensor, tau_lo: float,
                        tau_hi: float, beta_lo: float, beta_mid: float, beta_hi: float,
                        dev_err: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Eq. 3-4 in place on fp32 logits [rows][vocab] (row stride may exceed vocab)."""
-    if logits.dtype != torch.float32 or logits.dim() != 2 or logits.stride(1) != 1:
-        raise ValueError("logits must be fp32 [rows][vocab] with unit column stride")
-    if refl_ids.dtype != torch.int32 or reward.dtype != torch.float32:
-        raise ValueError("refl_ids int32, reward float32")
+    rows, vocab = _logit_rows(logits)
+    if refl_ids.dtype != torch.int32 or refl_ids.dim() != 1:
+        raise ValueError("refl_ids must be a 1-D int32 tensor")
+    _expect(reward, "reward", (rows,), torch.float32)
+    _expect_dev_err(dev_err)
     _need_cuda(refl_ids, reward, dev_err)
     _same_gpu(logits, reward)
-    rows, vocab = logits.shape
     st = load_library().reco_logit_penalty(_ptr(logits), rows, vocab, logits.stride(0), _ptr(refl_ids),
                                            refl_ids.numel(), _ptr(reward), tau_lo, tau_hi, beta_lo, beta_mid,
                                            beta_hi, _ptr(dev_err), _stream(logits.device))
@@ -330,23 +389,22 @@ def reco_penalty_sample(logits: torch.Tensor, refl_ids: Optional[torch.Tensor], 
                         ws: Optional[torch.Tensor] = None, dev_err: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Eq. 3-4 in place on fp32 logits [rows][vocab], then the next token of
     each row from softmax(z~ / T) (greedy when T = 0); returns tokens [rows] int32."""
-    if logits.dtype != torch.float32 or logits.dim() != 2 or logits.stride(1) != 1:
-        raise ValueError("logits must be fp32 [rows][vocab] with unit column stride")
-    if (refl_ids is not None and refl_ids.dtype != torch.int32) or reward.dtype != torch.float32:
-        raise ValueError("refl_ids int32, reward float32")
-    rows, vocab = logits.shape
-    if tokens is None and logits.is_cuda:
-        tokens = torch.empty(rows, dtype=torch.int32, device=logits.device)
-    if tokens is not None and tokens.dtype != torch.int32:
-        raise ValueError("tokens must be int32")
+    rows, vocab = _logit_rows(logits)
+    if refl_ids is not None and (refl_ids.dtype != torch.int32 or refl_ids.dim() != 1):
+        raise ValueError("refl_ids must be a 1-D int32 tensor")
+    _expect(reward, "reward", (rows,), torch.float32)
+    _expect(tokens, "tokens", (rows,), torch.int32)
+    _expect_dev_err(dev_err)
     _need_cuda(reward, refl_ids, tokens, ws, dev_err)
     _same_gpu(logits, reward)
+    if tokens is None:
+        tokens = torch.empty(rows, dtype=torch.int32, device=logits.device)
     ws = _ws(lambda: penalty_sample_workspace_size(rows, vocab), logits.device, ws)
     n_refl = 0 if refl_ids is None else refl_ids.numel()
     st = load_library().reco_penalty_sample(_ptr(logits), rows, vocab, logits.stride(0), _ptr(refl_ids), n_refl,
                                             _ptr(reward), tau_lo, tau_hi, beta_lo, beta_mid, beta_hi,
                                             float(temperature), int(seed) & (2 ** 64 - 1),
-                                            int(offset) & (2 ** 64 - 1), _ptr(tokens), _ptr(ws), ws.numel(),
+                                            int(offset) & (2 ** 64 - 1), _ptr(tokens), _ptr(ws), _nbytes(ws),
                                             _ptr(dev_err), _stream(logits.device))
     _check(st, "reco_penalty_sample")
     return tokens
@@ -356,17 +414,21 @@ def reco_answer_ppl(logits: torch.Tensor, tokens: torch.Tensor, tau_p: float, pp
                     stop: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
                     dev_err: Optional[torch.Tensor] = None):
     """Eq. 5-6: returns (ppl [B] fp32, stop [B] int32)."""
-    if logits.dtype != torch.float32 or logits.dim() != 3 or tokens.dtype != torch.int32:
-        raise ValueError("logits fp32 [B][n][V], tokens int32 [B][n]")
+    if logits.dtype != torch.float32 or logits.dim() != 3:
+        raise ValueError("logits must be fp32 [B][n][V]")
     B, n, V = logits.shape
+    _expect(tokens, "tokens", (B, n), torch.int32)
+    _expect(ppl, "ppl", (B,), torch.float32)
+    _expect(stop, "stop", (B,), torch.int32)
+    _expect_dev_err(dev_err)
+    _need_cuda(logits, tokens, ppl, stop, ws, dev_err)
     if ppl is None:
         ppl = torch.empty(B, dtype=torch.float32, device=logits.device)
     if stop is None:
         stop = torch.empty(B, dtype=torch.int32, device=logits.device)
-    _need_cuda(logits, tokens, ppl, stop, ws, dev_err)
     ws = _ws(lambda: answer_ppl_workspace_size(B, n, V), logits.device, ws)
     st = load_library().reco_answer_ppl(_ptr(logits), _ptr(tokens), B, n, V, tau_p, _ptr(ppl), _ptr(stop),
-                                        _ptr(ws), ws.numel(), _ptr(dev_err), _stream(logits.device))
+                                        _ptr(ws), _nbytes(ws), _ptr(dev_err), _stream(logits.device))
     _check(st, "reco_answer_ppl")
     return ppl, stop
 

@@ -2,10 +2,10 @@
 
 The paper's loop, per completed reasoning step i with process reward v_i:
 
-* reward-driven retention (Section 3.2, Eq. 1): once the cache has grown by
-  S tokens since the last compression, compress it to m_i = lambda_i * L
-  tokens, lambda_i set by the step's reward relative to the trajectory's own
-  reward statistics (or by the fixed map r = clamp(1 - v/2, 0.3, 1));
+* reward-driven retention (Section 3.2, Eq. 1 and its schedule): compress
+  when L - L_{i-1} >= S, down to m_i = lambda_i * L rows, where lambda_i
+  follows v_i measured against the trajectory's reward history (or the fixed
+  map r = clamp(1 - v/2, 0.3, 1));
 * attention-guided selection (Eq. 2) over the w most recent queries;
 * the reward band of the just-completed step sets the reflection-token
   penalty applied to every logit row of the next step (Eq. 3-4), and the

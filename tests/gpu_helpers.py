@@ -2,7 +2,8 @@
 results back as exact float64 arrays, and the comparison rules.
 
 Tolerances (written here once, used by every GPU test):
-* decode output, fp32 caches: |gpu - oracle| <= 1e-5 * max(1, max_d |oracle row|);
+* decode output, fp32 caches: |gpu - oracle| <= 1e-5 * max_d |oracle row| (per
+  query row; a 1e-7 floor only for rows that are exactly zero);
 * decode output, bf16 caches: |gpu - oracle| <= 2e-2 (fp32 accumulation, bf16 output);
 * decode log-sum-exp: 1e-5 absolute (fp32) and 1e-4 absolute (bf16 inputs);
 * scores: relative error <= SCORE_RTOL (a diagnostic bound; the kept-index
@@ -38,7 +39,7 @@ def upload(ci: I.CacheInputs, device="cuda"):
 def assert_decode_close(gpu_out: torch.Tensor, ref: np.ndarray, dtype: str, what: str = ""):
     g = f64(gpu_out)
     if dtype == "f32":
-        scale = np.maximum(1.0, np.abs(ref).max(axis=-1, keepdims=True))
+        scale = np.maximum(1e-7, np.abs(ref).max(axis=-1, keepdims=True))
         err = np.abs(g - ref) / scale
         assert err.max() <= 1e-5, f"{what}: fp32 decode rel err {err.max():.3e}"
     else:

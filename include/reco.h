@@ -208,6 +208,24 @@ reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int
                                float *row_stats, void *ws, size_t ws_bytes, int32_t *dev_err,
                                hipStream_t stream);
 
+/* reco_decode_attn for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same computation, arguments and errors as reco_decode_attn, without the
+ * workspace: the split partials go to a static array inside the library
+ * (8 MiB on each device it runs on, held until the process ends), so the call
+ * allocates nothing and the caller passes only inputs and outputs.  Every call
+ * on one device shares that array and the array keeps the last call's
+ * contents (no call depends on them): calls that overlap on one device race,
+ * so serialise them (one stream, or events).  Returns RECO_ERR_WORKSPACE if
+ * the call would need more than 8 MiB of partials (a call needs at most
+ * compute_units * (16 * head_dim + 32) * 4 bytes, 2.1 MB on a 256-CU MI355X),
+ * and RECO_ERR_HIP if the array's device address cannot be looked up; the
+ * device current at the call must be the one `stream` belongs to. */
+reco_status_t reco_decode_attn_noalloc(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,
+                                       const void *q, int32_t n_q_heads, float scale, const void *k_new,
+                                       const void *v_new, void *out, float *lse, float *row_stats,
+                                       int32_t *dev_err, hipStream_t stream);
+
 /* ------------------------------------------------------------------------ */
 /* Eq. 3 and Eq. 4 (Section 3.3, reward-banded reflection penalty): for every
  * row b, beta_b = beta_lo if reward[b] <= tau_lo, beta_hi if

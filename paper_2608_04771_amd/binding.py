@@ -34,7 +34,7 @@ DEV_ERRORS = {0: "ok", 1: "append overflow", 2: "bad retention", 3: "bad score",
 EXPORTED = [
     "reco_score_workspace_size", "reco_score", "reco_select_compact_workspace_size", "reco_select_compact",
     "reco_pool_scores", "reco_layer_retention",
-    "reco_decode_attn_workspace_size", "reco_decode_attn", "reco_logit_penalty",
+    "reco_decode_attn_workspace_size", "reco_decode_attn", "reco_decode_attn_noalloc", "reco_logit_penalty",
     "reco_penalty_sample_workspace_size", "reco_penalty_sample",
     "reco_answer_ppl_workspace_size", "reco_answer_ppl", "reco_retention_from_reward", "reco_retention_eq1",
     "reco_kept_count", "reco_status_str", "reco_abi_version",
@@ -70,6 +70,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "reco_layer_retention": (F64, [F64, I32, I32, F64]),
         "reco_decode_attn_workspace_size": (SZ, [C, I32, I32]),
         "reco_decode_attn": (I32, [C, I32, I32, P, I32, F32, P, P, P, P, P, P, SZ, P, P]),
+        "reco_decode_attn_noalloc": (I32, [C, I32, I32, P, I32, F32, P, P, P, P, P, P, P]),
         "reco_logit_penalty": (I32, [P, I32, I32, I64, P, I32, P, F32, F32, F32, F32, F32, P, P]),
         "reco_penalty_sample_workspace_size": (SZ, [I32, I32]),
         "reco_penalty_sample": (I32, [P, I32, I32, I64, P, I32, P, F32, F32, F32, F32, F32, F32, U64, U64, P, P, SZ,
@@ -355,6 +356,28 @@ def reco_decode_attn(cache: KVCache, q: torch.Tensor, k_new: Optional[torch.Tens
                                          _ptr(out), _ptr(lse), _ptr(row_stats), _ptr(ws), _nbytes(ws),
                                          _ptr(dev_err), _stream(q.device))
     _check(st, "reco_decode_attn")
+    return out, lse
+
+
+def reco_decode_attn_noalloc(cache: KVCache, q: torch.Tensor, out: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                             k_new: Optional[torch.Tensor] = None, v_new: Optional[torch.Tensor] = None,
+                             scale: Optional[float] = None, layer0: int = 0, n_layers: Optional[int] = None,
+                             dev_err: Optional[torch.Tensor] = None, row_stats: Optional[torch.Tensor] = None):
+    """reco_decode_attn without a workspace and without any allocation: the
+    caller passes ``out`` (and optionally ``lse``); the split partials live in
+    the library's static per-device array.  Calls overlapping on one GPU race."""
+    layer0, nl = _layers(cache, layer0, n_layers)
+    if out is None:
+        raise ValueError("out must be given (this entry point allocates nothing)")
+    _decode_shapes(cache, nl, q, k_new, v_new, out, lse, row_stats)
+    _expect_dev_err(dev_err)
+    _need_cuda(cache.k, q, k_new, v_new, out, lse, dev_err, row_stats)
+    D = cache.shape[4]
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    st = load_library().reco_decode_attn_noalloc(cache.ref(), layer0, nl, _ptr(q), q.shape[2], scale, _ptr(k_new),
+                                                 _ptr(v_new), _ptr(out), _ptr(lse), _ptr(row_stats), _ptr(dev_err),
+                                                 _stream(q.device))
+    _check(st, "reco_decode_attn_noalloc")
     return out, lse
 
 

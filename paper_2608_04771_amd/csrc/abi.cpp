@@ -247,10 +247,17 @@ size_t reco_decode_attn_workspace_size(const reco_kv_cache_t *cache, int32_t n_l
   return reco::decode_workspace_bytes(units, cache->capacity, cache->head_dim, current_compute_units());
 }
 
-reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers, const void *q,
-                               int32_t n_q_heads, float scale, const void *k_new, const void *v_new, void *out,
-                               float *lse, float *row_stats, void *ws, size_t ws_bytes, int32_t *dev_err,
-                               hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared by both decode entry points: host validation, then the launch with
+// the split partials in `ws` (caller workspace) or, when `ws` is null, in the
+// library's static per-device scratch array.
+reco_status_t decode_common(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers, const void *q,
+                            int32_t n_q_heads, float scale, const void *k_new, const void *v_new, void *out,
+                            float *lse, float *row_stats, void *ws, size_t ws_bytes, bool use_scratch,
+                            int32_t *dev_err, hipStream_t stream) {
   if (!cache_ok(cache) || !q || !out) return RECO_ERR_INVALID_ARG;
   if ((k_new == nullptr) != (v_new == nullptr)) return RECO_ERR_INVALID_ARG;
   if (!layers_ok(cache, layer0, n_layers) || !units_ok(cache, n_layers) || !isfinite(scale))
@@ -262,8 +269,14 @@ reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int
   if (G > 16) return RECO_ERR_UNSUPPORTED;
   const int units = n_layers * cache->batch * cache->n_kv_heads;
   const int cus = current_compute_units();
-  const size_t need = reco::decode_workspace_bytes(units, cache->capacity, cache->head_dim, cus);
-  if (!ws || ws_bytes < need) return RECO_ERR_WORKSPACE;
+  if (use_scratch) {
+    if (reco::decode_scratch_bytes(units, cache->capacity, cache->head_dim, cus) > reco::kDecodeScratchBytes)
+      return RECO_ERR_WORKSPACE;
+    if (reco::decode_scratch(&ws) != hipSuccess) return RECO_ERR_HIP;
+  } else {
+    const size_t need = reco::decode_workspace_bytes(units, cache->capacity, cache->head_dim, cus);
+    if (!ws || ws_bytes < need) return RECO_ERR_WORKSPACE;
+  }
 
   reco::DecodeParams p{};
   p.k = cache->k;
@@ -288,6 +301,26 @@ reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int
   p.hq = n_q_heads;
   p.scale_log2 = scale * 1.4426950408889634f;
   return hip_status(reco::launch_decode(p, cache->dtype, cache->head_dim, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers, const void *q,
+                               int32_t n_q_heads, float scale, const void *k_new, const void *v_new, void *out,
+                               float *lse, float *row_stats, void *ws, size_t ws_bytes, int32_t *dev_err,
+                               hipStream_t stream) {
+  return decode_common(cache, layer0, n_layers, q, n_q_heads, scale, k_new, v_new, out, lse, row_stats, ws,
+                       ws_bytes, false, dev_err, stream);
+}
+
+reco_status_t reco_decode_attn_noalloc(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers, const void *q,
+                                       int32_t n_q_heads, float scale, const void *k_new, const void *v_new,
+                                       void *out, float *lse, float *row_stats, int32_t *dev_err,
+                                       hipStream_t stream) {
+  return decode_common(cache, layer0, n_layers, q, n_q_heads, scale, k_new, v_new, out, lse, row_stats, nullptr,
+                       0, true, dev_err, stream);
 }
 
 // ---------------------------------------------------------------- penalty

@@ -27,6 +27,9 @@
 
 #include <math.h>
 
+#include <atomic>
+#include <mutex>
+
 namespace reco {
 
 namespace {
@@ -621,6 +624,43 @@ int decode_splits(int units, int capacity, int compute_units) {
 size_t decode_workspace_bytes(int units, int capacity, int head_dim, int compute_units) {
   const size_t splits = static_cast<size_t>(decode_splits(units, capacity, compute_units));
   return static_cast<size_t>(units) * splits * (16 * static_cast<size_t>(head_dim) + 32) * sizeof(float);
+}
+
+size_t decode_scratch_bytes(int units, int capacity, int head_dim, int compute_units) {
+  if (decode_splits(units, capacity, compute_units) == 1) return 0;   // finalised in place, no partials
+  return decode_workspace_bytes(units, capacity, head_dim, compute_units);
+}
+
+// Split partials of the allocation-free entry point.  Every device holds its
+// own copy of this array at its own address until the process ends.  In host
+// code `scratch` names a host-side stand-in for the device symbol, not device
+// memory: host code uses only the address hipGetSymbolAddress returns for the
+// current device, never the name itself.  The decode kernels write every
+// partial they later read, so the array never needs clearing; calls that
+// overlap on one device share it and race.
+static __device__ __align__(256) unsigned char scratch[kDecodeScratchBytes];
+
+hipError_t decode_scratch(void **ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<void *> addr[kMaxDevices];
+  static std::mutex mu;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void *p = addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(mu);
+    p = addr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));   // with `dev` current
+      if (e != hipSuccess) return e;
+      if (!p) return hipErrorInvalidSymbol;
+      addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *ptr = p;
+  return hipSuccess;
 }
 
 hipError_t launch_decode(const DecodeParams &p, int dtype, int head_dim, hipStream_t s) {

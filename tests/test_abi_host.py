@@ -169,6 +169,27 @@ def test_decode_rejects_bad_arguments():
     assert call(wsb=8) == B.RECO_ERR_WORKSPACE
 
 
+def test_decode_noalloc_rejects_bad_arguments():
+    """The allocation-free decode validates exactly like reco_decode_attn
+    (every case here is refused before any HIP call)."""
+    lib = B.load_library()
+    c = _fake_cache()
+
+    def call(cache=c, nl=2, q=0x10, hq=4, scale=0.1, kn=None, vn=None, out=0x50):
+        return lib.reco_decode_attn_noalloc(ctypes.byref(cache), 0, nl, P(q), hq, scale, P(kn) if kn else None,
+                                            P(vn) if vn else None, P(out), None, None, None, None)
+    assert call(q=0) == B.RECO_ERR_INVALID_ARG
+    assert call(out=0) == B.RECO_ERR_INVALID_ARG
+    assert call(kn=0x60) == B.RECO_ERR_INVALID_ARG                        # k_new without v_new
+    assert call(vn=0x60) == B.RECO_ERR_INVALID_ARG
+    assert call(nl=3) == B.RECO_ERR_INVALID_ARG
+    assert call(hq=5) == B.RECO_ERR_INVALID_ARG
+    assert call(scale=float("nan")) == B.RECO_ERR_INVALID_ARG
+    assert call(cache=_fake_cache(k=0)) == B.RECO_ERR_INVALID_ARG
+    assert call(hq=2 * 17) == B.RECO_ERR_UNSUPPORTED                      # G = 17 > 16
+    assert call(cache=_fake_cache(head_dim=96)) == B.RECO_ERR_UNSUPPORTED
+
+
 def test_penalty_and_ppl_reject_bad_arguments():
     lib = B.load_library()
     pen = lambda logits=0x10, rows=1, vocab=100, ld=100, ids=0x20, n=4, rew=0x30: lib.reco_logit_penalty(  # noqa: E731

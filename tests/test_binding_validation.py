@@ -79,8 +79,8 @@ def test_pool_arguments():
     _raises("GPU", B.reco_pool_scores, c, s, W, 5, pooled=_z(NL, BS, H, CAP))
 
 
-def test_decode_arguments():
-    fn = B.reco_decode_attn
+@pytest.mark.parametrize("fn", [B.reco_decode_attn, B.reco_decode_attn_noalloc])
+def test_decode_arguments(fn):
     c = _cache()
     q = _z(NL, BS, HQ, D, dtype=BF)
     out = torch.empty_like(q)
@@ -101,6 +101,11 @@ def test_decode_arguments():
     _raises("row_stats", call, row_stats=_z(NL, BS, HQ, 2, dtype=F64))
     _raises("dev_err", call, dev_err=_z(0, dtype=I32))
     _raises("GPU", call, k_new=kn, v_new=kn, lse=_z(NL, BS, HQ), row_stats=_z(NL, BS, HQ, 2))
+
+
+def test_decode_noalloc_needs_out():
+    c = _cache()
+    _raises("out must be given", B.reco_decode_attn_noalloc, c, _z(NL, BS, HQ, D, dtype=BF), None)
 
 
 def test_logit_arguments():

@@ -1,8 +1,10 @@
 /*
  * Plain C11 client of libreco.so: one compression (Eq. 2 scoring, then
  * reward-budgeted selection and in-place compaction, Section 3.2) followed by
- * decode steps that append their token, driven only through the C ABI in
- * reco.h with memory from the HIP runtime (no Python, no torch).
+ * decode steps that append their token, then the banded reflection penalty on
+ * a block of logit rows (Eq. 3-4) and the answer perplexity with its stop
+ * flag (Eq. 5-6): all five calls driven only through the C ABI in reco.h with
+ * memory from the HIP runtime (no Python, no torch).
  *
  * Usage: reco_c_driver <input file> <output file>
  *
@@ -14,6 +16,11 @@
  *   elem   K[NL][B][H][cap][D], V[NL][B][H][cap][D]
  *   elem   q_win[NL][B][Hq][w][D]
  *   elem   q[nsteps][NL][B][Hq][D], k_new[nsteps][NL][B][H][D], v_new[nsteps][NL][B][H][D]
+ *   int32  rows, vocab, n_refl
+ *   float  tau_lo, tau_hi, beta_lo, beta_mid, beta_hi
+ *   float  logits[rows][vocab];  int32 refl_ids[n_refl];  float reward[rows]
+ *   int32  pb, pn, pv;  float tau_p
+ *   float  answer_logits[pb][pn][pv];  int32 answer_tokens[pb][pn]
  * (elem = 4-byte float for fp32, the 2-byte bf16 pattern for bf16)
  *
  * Output:
@@ -23,6 +30,8 @@
  *   int32  len[NL][B][H]                (after the decode steps)
  *   elem   out[nsteps][NL][B][Hq][D]
  *   float  lse[nsteps][NL][B][Hq]
+ *   float  logits[rows][vocab]          (after the penalty, in place)
+ *   float  ppl[pb];  int32 stop[pb]
  *
  * Every HIP and library status is checked; any failure prints a message and
  * exits with status 1 before the output file is written.
@@ -132,6 +141,29 @@ int main(int argc, char **argv) {
   void *d_q = upload(in, (size_t)nsteps * qrows * D * e, "q");
   void *d_kn = upload(in, (size_t)nsteps * units * D * e, "k_new");
   void *d_vn = upload(in, (size_t)nsteps * units * D * e, "v_new");
+  int32_t phdr[3];
+  float pen[5];
+  read_exact(in, phdr, sizeof phdr, "penalty header");
+  read_exact(in, pen, sizeof pen, "penalty bands");
+  const int32_t rows = phdr[0], vocab = phdr[1], n_refl = phdr[2];
+  if (rows < 1 || vocab < 1 || n_refl < 0) {
+    fprintf(stderr, "bad penalty header\n");
+    return 1;
+  }
+  float *d_logits = (float *)upload(in, (size_t)rows * vocab * sizeof(float), "logits");
+  int32_t *d_refl = (int32_t *)upload(in, (size_t)n_refl * sizeof(int32_t), "refl_ids");
+  float *d_reward = (float *)upload(in, (size_t)rows * sizeof(float), "reward");
+  int32_t ahdr[3];
+  float tau_p;
+  read_exact(in, ahdr, sizeof ahdr, "answer header");
+  read_exact(in, &tau_p, sizeof tau_p, "tau_p");
+  const int32_t pb = ahdr[0], pn = ahdr[1], pv = ahdr[2];
+  if (pb < 1 || pn < 1 || pv < 1) {
+    fprintf(stderr, "bad answer header\n");
+    return 1;
+  }
+  float *d_alog = (float *)upload(in, (size_t)pb * pn * pv * sizeof(float), "answer logits");
+  int32_t *d_atok = (int32_t *)upload(in, (size_t)pb * pn * sizeof(int32_t), "answer tokens");
   fclose(in);
 
   reco_kv_cache_t cache;
@@ -188,6 +220,22 @@ int main(int argc, char **argv) {
     RECO_CHECK(reco_decode_attn(&cache, 0, NL, q, Hq, scale, kn, vn, out, lse, NULL, ws_dec, ws_dec_bytes, d_err,
                                 stream));
   }
+  /* Eq. 3-4 on the logit rows (in place), then Eq. 5-6 on the answer probe. */
+  RECO_CHECK(reco_logit_penalty(d_logits, rows, vocab, vocab, d_refl, n_refl, d_reward, pen[0], pen[1], pen[2],
+                                pen[3], pen[4], d_err, stream));
+  float *d_ppl = NULL;
+  int32_t *d_stop = NULL;
+  HIP_CHECK(hipMalloc((void **)&d_ppl, (size_t)pb * sizeof(float)));
+  HIP_CHECK(hipMalloc((void **)&d_stop, (size_t)pb * sizeof(int32_t)));
+  const size_t ws_ppl_bytes = reco_answer_ppl_workspace_size(pb, pn, pv);
+  if (!ws_ppl_bytes) {
+    fprintf(stderr, "the answer-ppl workspace query refused the shape\n");
+    return 1;
+  }
+  void *ws_ppl = NULL;
+  HIP_CHECK(hipMalloc(&ws_ppl, ws_ppl_bytes));
+  RECO_CHECK(reco_answer_ppl(d_alog, d_atok, pb, pn, pv, tau_p, d_ppl, d_stop, ws_ppl, ws_ppl_bytes, d_err,
+                             stream));
   HIP_CHECK(hipStreamSynchronize(stream));
 
   FILE *outf = fopen(argv[2], "wb");
@@ -201,13 +249,16 @@ int main(int argc, char **argv) {
   download(outf, d_len, units * sizeof(int32_t));
   download(outf, d_out, (size_t)nsteps * qrows * D * e);
   download(outf, d_lse, (size_t)nsteps * qrows * sizeof(float));
+  download(outf, d_logits, (size_t)rows * vocab * sizeof(float));
+  download(outf, d_ppl, (size_t)pb * sizeof(float));
+  download(outf, d_stop, (size_t)pb * sizeof(int32_t));
   if (fclose(outf) != 0) {
     perror(argv[2]);
     return 1;
   }
 
   void *bufs[] = {d_ret, d_len, d_k, d_v, d_qwin, d_q, d_kn, d_vn, d_err, d_scores, d_kept, d_out, d_lse,
-                  ws_score, ws_sel, ws_dec};
+                  ws_score, ws_sel, ws_dec, d_logits, d_refl, d_reward, d_alog, d_atok, d_ppl, d_stop, ws_ppl};
   for (size_t i = 0; i < sizeof bufs / sizeof bufs[0]; ++i) HIP_CHECK(hipFree(bufs[i]));
   HIP_CHECK(hipStreamDestroy(stream));
   return 0;

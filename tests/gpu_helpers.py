@@ -6,8 +6,10 @@ Tolerances (written here once, used by every GPU test):
   query row; a 1e-7 floor only for rows that are exactly zero);
 * decode output, bf16 caches: |gpu - oracle| <= 2e-2 (fp32 accumulation, bf16 output);
 * decode log-sum-exp: 1e-5 absolute (fp32) and 1e-4 absolute (bf16 inputs);
-* scores: relative error <= SCORE_RTOL (a diagnostic bound; the kept-index
-  check below is the contract);
+* scores: relative error <= SCORE_RTOL everywhere (a diagnostic bound), and
+  <= THETA_RTOL for the prefix scores within 10% of the oracle's k-th prefix
+  score theta, the precision the tie rule below relies on (neighbouring
+  scores near theta sit about 1e-5 apart, ties are excused within 1e-6);
 * kept indices: equal sets except positions whose oracle score lies within
   1e-6 relative of the oracle's k-th prefix score (ties);
 * gathered K/V rows and appended rows: bit-exact.
@@ -22,7 +24,11 @@ from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd import inputs as I
 
 SCORE_RTOL = 2e-6
+THETA_RTOL = 5e-7
 TIE_RTOL = 1e-6
+
+# Worst near-theta score error seen in this process (printed by the tests).
+WORST_NEAR_THETA = {"rel": 0.0, "where": ""}
 
 
 def f64(t: torch.Tensor) -> np.ndarray:
@@ -80,3 +86,28 @@ def kept_sets_match(idx_gpu: np.ndarray, s_or: np.ndarray, L: int, w: int, r: fl
     if bad:
         return False, f"unexcused swaps {bad[:5]} theta={theta} scores={[s_or[j] for j in bad[:5]]}"
     return True, f"{len(diff)} excused tie swaps"
+
+
+def assert_theta_precision(s_gpu: np.ndarray, s_or: np.ndarray, L: int, w: int, r: float, what: str = ""):
+    """Relative error of the GPU prefix scores within 10% of theta, the
+    oracle's k-th largest prefix score at retention r (k = m - min(w, L)),
+    must stay within THETA_RTOL.  Returns (worst error, number of scores
+    checked); units with nothing to select from the prefix are skipped."""
+    w_eff = min(w, L)
+    P = L - w_eff
+    k = oracle.kept_count(L, w, r) - w_eff
+    if P <= 0 or k <= 0:
+        return 0.0, 0
+    pre_or = np.asarray(s_or[:P], dtype=np.float64)
+    pre_gpu = np.asarray(s_gpu[:P], dtype=np.float64)
+    theta = np.sort(pre_or)[::-1][k - 1]
+    near = np.abs(pre_or - theta) <= 0.1 * theta
+    if theta <= 0 or not near.any():
+        return 0.0, 0
+    rel = np.abs(pre_gpu[near] - pre_or[near]) / pre_or[near]
+    worst = float(rel.max())
+    if worst > WORST_NEAR_THETA["rel"]:
+        WORST_NEAR_THETA.update(rel=worst, where=what)
+    assert worst <= THETA_RTOL, f"{what}: score rel err near theta {worst:.3e} > {THETA_RTOL:.0e} (theta={theta:.6e})"
+    return worst, int(near.sum())
+

@@ -7,7 +7,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import SCORE_RTOL, assert_decode_close, assert_lse_close, f64, kept_sets_match, upload
+from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_theta_precision, f64,
+                         kept_sets_match, upload)
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd import inputs as I
 
@@ -40,6 +41,7 @@ def test_tiny_workload_full_loop():
         L = int(ci.seq_len[0])
         ok, msg = kept_sets_match(kept[0, 0, h], s_or[0, 0, h], L, wl.window, r[0])
         assert ok, msg
+        assert_theta_precision(s_gpu[0, 0, h], s_or[0, 0, h], L, wl.window, r[0], f"tiny loop head {h}")
         exact = exact and msg == "exact"
         m = len(idx_or[(0, 0, h)])
         if msg != "exact":
@@ -78,6 +80,7 @@ def test_7b16k_full_size_sampled():
         s_or = oracle.score_unit(Kf, f64(ci.q_win[l, b, h * G:(h + 1) * G]), scale)
         rel = np.abs(s_gpu[l, b, h, :L] - s_or) / s_or
         assert rel.max() <= SCORE_RTOL, rel.max()
+        assert_theta_precision(s_gpu[l, b, h], s_or, L, wl.window, float(r[0]), f"7b unit {(l, b, h)}")
         ok, msg = kept_sets_match(kept[l, b, h], s_or, L, wl.window, float(r[0]))
         assert ok, msg
         idx = torch.from_numpy(kept[l, b, h, :m].astype(np.int64)).cuda()
@@ -119,5 +122,6 @@ def test_7b16k_full_size_sampled():
     for (l, b, h) in units:
         s_or = oracle.score_unit(f64(cache.k[l, b, h, :n]), f64(q_win[l, b, h * G:(h + 1) * G]), scale)
         assert (np.abs(s_fed[l, b, h, :n] - s_or) / s_or).max() <= SCORE_RTOL
+        assert_theta_precision(s_fed[l, b, h], s_or, n, w, 0.5, f"7b one-pass unit {(l, b, h)}")
         ok, msg = kept_sets_match(oracle.select_unit(s_fed[l, b, h], n, w, 0.5), s_or, n, w, 0.5)
         assert ok, msg

@@ -4,7 +4,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import SCORE_RTOL, f64, kept_sets_match, upload
+from gpu_helpers import WORST_NEAR_THETA, SCORE_RTOL, assert_theta_precision, f64, kept_sets_match, upload
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd import inputs as I
 
@@ -32,6 +32,8 @@ def _score_check(cache_in, q_win, w, causal=True, D=None):
         worst = max(worst, float(rel[big].max()) if big.any() else 0.0)
         G = q_win.shape[2] // lens.shape[2]
         assert abs(g[u][:L].sum() - G * min(w, L)) <= 1e-4 * G * min(w, L)     # mass invariant
+        for r in (0.5, 0.75, 0.9):                                             # the workloads' retention range
+            assert_theta_precision(g[u], ref[u], L, w, r, f"unit {u} r={r}")
     assert worst <= SCORE_RTOL, f"score rel err {worst:.3e}"
     return s, ref, worst
 
@@ -60,7 +62,8 @@ def test_score_ragged(dtype, D, G, w, causal):
     q = torch.randn((NL, Bsz, H * G, w, D), generator=gen).to(td)
     cache = B.KVCache(k.cuda(), v.cuda(), ln.cuda())
     _, _, worst = _score_check(cache, q, w, causal)
-    print(f"{dtype} D={D} G={G} w={w} causal={causal} max rel err {worst:.3e}")
+    print(f"{dtype} D={D} G={G} w={w} causal={causal} max rel err {worst:.3e}; worst near theta so far "
+          f"{WORST_NEAR_THETA['rel']:.3e} ({WORST_NEAR_THETA['where']})")
 
 
 def test_select_compact_tiny_end_to_end():

@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import SCORE_RTOL, f64, kept_sets_match
+from gpu_helpers import SCORE_RTOL, assert_theta_precision, f64, kept_sets_match
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd import inputs as I
 
@@ -110,3 +110,4 @@ def test_stats_fed_score_matches_oracle(dtype, D, G, w, prompt):
             kept = oracle.select_unit(a[u], L, w, r)                       # GPU scores, oracle's selection rule
             ok, msg = kept_sets_match(kept, ref, L, w, r)
             assert ok, (u, r, msg)
+            assert_theta_precision(a[u], ref, L, w, r, f"one-pass unit {u} r={r}")

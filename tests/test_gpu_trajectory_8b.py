@@ -14,7 +14,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import SCORE_RTOL, assert_decode_close, assert_lse_close, f64, kept_sets_match
+from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_theta_precision, f64,
+                         kept_sets_match)
 from paper_2608_04771_amd import inputs as I
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd.controller import RecoDecoder, RecoPolicy
@@ -89,6 +90,7 @@ def test_8b_trajectory_full_size():
                         s_or = oracle.score_unit(K0, win[l, b, h * G:(h + 1) * G], scale)
                         s_gpu = dec.scores[u][:L].cpu().numpy().astype(np.float64)
                         assert (np.abs(s_gpu - s_or) / s_or).max() <= SCORE_RTOL
+                        assert_theta_precision(s_gpu, s_or, L, w, r, f"8b step {bi} unit {u}")
                         kept = dec.kept[u].cpu().numpy()
                         ok, msg = kept_sets_match(kept, s_or, L, w, r)
                         assert ok, (bi, u, msg)

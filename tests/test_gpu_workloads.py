@@ -11,7 +11,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import SCORE_RTOL, assert_decode_close, assert_lse_close, f64, kept_sets_match
+from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_theta_precision, f64,
+                         kept_sets_match)
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd import inputs as I
 
@@ -54,6 +55,7 @@ def _run_workload(wl, units, decode_steps, check_steps, seq_lens=None):
         s_gpu = scores[u][:L].cpu().numpy().astype(np.float64)
         rel = np.abs(s_gpu - s_or) / s_or
         assert rel.max() <= SCORE_RTOL, (u, rel.max())
+        assert_theta_precision(s_gpu, s_or, L, wl.window, r[u[1]], f"{wl.name} unit {u}")
         ok, msg = kept_sets_match(kept[u].cpu().numpy(), s_or, L, wl.window, r[u[1]])
         assert ok, (u, msg)
         m = int(lens1[u])

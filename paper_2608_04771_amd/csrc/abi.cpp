@@ -155,6 +155,8 @@ reco_status_t reco_score(const reco_kv_cache_t *cache, int32_t layer0, int32_t n
   p.rows = G * w;
   p.rows_pad = (p.rows + 15) / 16 * 16;
   p.chunks = (cache->capacity + reco::kScoreChunk - 1) / reco::kScoreChunk;
+  p.chunk_keys = reco::kScoreChunk;
+  p.cus = current_compute_units();
   p.row_part = reinterpret_cast<float *>(ws);
   p.row_stat = p.row_part + static_cast<size_t>(units) * p.chunks * p.rows_pad * 2;
   p.given = row_stats;

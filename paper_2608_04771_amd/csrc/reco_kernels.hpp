@@ -21,10 +21,12 @@ struct ScoreParams {
   const float *given;     // nullable [n_layers][batch][hq][w][2] window-row (max, sum) from decode
   int32_t *dev_err;
   int layer0, n_layers, batch, hkv, cap, group, hq, w, rows, rows_pad, chunks;
+  int chunk_keys;         // keys per work item (set by launch_score; chunks = ceil(cap / chunk_keys))
+  int cus;                // compute units of the device (persistent grids)
   int causal;
   float scale_log2;
 };
-constexpr int kScoreChunk = 512;      // keys per workgroup
+constexpr int kScoreChunk = 512;      // keys per workgroup of the row-split kernels (workspace sizing)
 constexpr int kScoreMaxRows = 4096;   // G * w limit
 size_t score_workspace_bytes(int units, int capacity, int rows);
 hipError_t launch_score(const ScoreParams &p, int dtype, int head_dim, hipStream_t s);

@@ -10,6 +10,22 @@ One step = one pass of the whole path over one batch of synthetic input:
 Every step starts from its own pristine copy of the cache, staged in HBM
 before the timed region.  Prints one JSON line (rank 0, N = 1).
 
+The other workloads (`--workload`):
+  7b-batch32     32 ragged sequences (4K-32K tokens) of the 7B shape: one
+                 compression, then 256 decode calls over all layers; the cache
+                 is restored from a pristine copy between steps (untimed).
+  32b64k         the 32B shape (64 layers, 8 x 65,536 tokens): four rounds of
+                 (compression -> 64 decode calls, the rows' penalty and
+                 sampling on a side stream), rounds 2-4 scored in one pass
+                 with the decode statistics, then the answer probe; the cache
+                 is regenerated from its seed between steps (untimed).
+  8b-trajectory  the 8B shape through the controller: a 512-token prompt and
+                 32,768 generated tokens, a compression at every reasoning
+                 step boundary and the penalty and sampling on every token.
+  tiny           the small fp32 parity case.
+For these, each step is timed on its own between device synchronisations
+and ms_per_step is their mean.
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 7b16k] [--no-cpu-baseline] [--no-extras]
 """
 from __future__ import annotations
@@ -347,14 +363,583 @@ def _cpu_baseline_sample(w: Workload, oracle, comp_budget_s: float, dec_budget_s
                        f"({est_step_s:.1f} s estimated)")}
 
 
+# ---------------------------------------------------------------------------
+# The larger workloads: shared accounting
+# ---------------------------------------------------------------------------
+
+def compress_bytes(lens0: np.ndarray, m: np.ndarray, moved_rows: int, Bsz: int, Hq: int, w: int, D: int, e: int,
+                   stats_fed: bool = False):
+    """Algorithmic bytes of one compression: one pass over K (Eq. 2), the
+    window queries (or their decode statistics), the scores written and read
+    back by the selection, the kept lists, and the moved K/V rows (read and
+    written)."""
+    NL = lens0.shape[0]
+    rows = int(lens0.sum())
+    win = NL * Bsz * Hq * w * (8 if stats_fed else 0) + NL * Bsz * Hq * w * D * e
+    return {"score": rows * D * e + win + rows * 4, "select": rows * 4 + int(m.sum()) * 4,
+            "compact": moved_rows * 2 * 2 * D * e}
+
+
+def decode_call_bytes(rows_attended: int, units: int, q_rows: int, D: int, e: int):
+    """Algorithmic bytes of one decode call: the K/V rows attended (cached and
+    new), the queries, outputs and log-sum-exps, and the appended rows."""
+    return rows_attended * 2 * D * e + 2 * q_rows * D * e + q_rows * 4 + 2 * units * D * e
+
+
+def moved_rows_of(kept: torch.Tensor, m: np.ndarray) -> int:
+    """Kept rows whose position changes in the compaction (kept[u][p] != p)."""
+    kk = kept.cpu().numpy()
+    moved = 0
+    for u in np.ndindex(*m.shape):
+        mu = int(m[u])
+        moved += int((kk[u][:mu] != np.arange(mu)).sum())
+    return moved
+
+
+def roofline_obj(kernel: str, bytes_per_launch: float, avg_ms: float, traffic=None):
+    achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9
+    return {"kernel": kernel, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic,
+            "traffic_unit": "bytes per decode_split_kernel launch", "algorithmic_bytes_per_launch": bytes_per_launch,
+            "avg_launch_ms": avg_ms}
+
+
+def host_threads():
+    """(threads for the oracle's BLAS pool, affinity core count): the cores
+    this process may run on, capped by the job's thread budget."""
+    affinity = len(os.sched_getaffinity(0))
+    budget = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    return (min(affinity, budget) if budget > 0 else affinity), affinity
+
+
+def oracle_unit_rates(samples_c, samples_d, scale: float, w: int, comp_budget_s: float, dec_budget_s: float):
+    """Time the oracle on sampled units: `samples_c` yields (K, V, Qwin, r)
+    host fp64 arrays of whole units to compress (score, select, compact),
+    `samples_d` yields (K, V, n, Q, k_new, v_new) decode steps.  Each phase
+    runs until its budget is used.  Returns seconds per cached row for each
+    phase, the counts, and the busy-thread average."""
+    import oracle
+    t_c = rows_c = n_c = 0
+    cpu = 0.0
+    for (K, V, Qw, r) in samples_c:
+        c0, t0 = time.process_time(), time.perf_counter()
+        s = oracle.score_unit(K, Qw, scale)
+        idx = oracle.select_unit(s, K.shape[0], w, r)
+        oracle.compact_unit(K, V, idx)
+        t_c += time.perf_counter() - t0
+        cpu += time.process_time() - c0
+        rows_c += K.shape[0]
+        n_c += 1
+        if t_c >= comp_budget_s:
+            break
+    t_d = rows_d = n_d = 0
+    for (K, V, n, Q, kn, vn) in samples_d:
+        c0, t0 = time.process_time(), time.perf_counter()
+        oracle.decode_unit(K, V, n, Q, scale, kn, vn)
+        t_d += time.perf_counter() - t0
+        cpu += time.process_time() - c0
+        rows_d += n + 1
+        n_d += 1
+        if t_d >= dec_budget_s:
+            break
+    return {"s_per_row_compress": t_c / max(rows_c, 1), "s_per_row_decode": t_d / max(rows_d, 1),
+            "units_compressed": n_c, "decode_samples": n_d, "t_compress": t_c, "t_decode": t_d,
+            "busy": cpu / max(t_c + t_d, 1e-9)}
+
+
+def emit_line(args, wl, value, ms_per_step, step_bytes, extra, cfg_extra):
+    res = {
+        "metric": METRIC, "value": value, "unit": "KV tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": dict({"workload": wl.name, "n_layers": wl.n_layers, "q_heads": wl.n_q_heads,
+                        "kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim, "window": wl.window,
+                        "seed": wl.seed}, **cfg_extra),
+        "achieved_GBps": step_bytes / (ms_per_step * 1e-3) / 1e9,
+        "pct_of_peak_hbm": 100.0 * step_bytes / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+        "algorithmic_bytes_per_step": step_bytes,
+        "timing": "each step timed on its own between device synchronisations; cache restores between steps "
+                  "are untimed",
+    }
+    res.update(extra)
+    print(json.dumps(res), flush=True)
+
+
+DECODE_KERNELS = "reco_decode_attn (decode_split_kernel, and decode_merge_kernel where a unit is split)"
+
+
+def timed_steps(args, restore, step):
+    """Warm-up then timed steps; restore() runs untimed before every step.
+    The first warm-up step (warm == 0) also records the step's sizes, so at
+    least one is run.  Returns the per-step wall times (ms) and the events of
+    the timed steps."""
+    if args.warmup < 1:
+        log("these workloads record their sizes in a warm-up step: running one")
+        args.warmup = 1
+    for i in range(args.warmup):
+        restore()
+        torch.cuda.synchronize()
+        step(None, warm=i)
+        torch.cuda.synchronize()
+    times, evs = [], []
+    for i in range(args.steps):
+        restore()
+        torch.cuda.synchronize()
+        ev = {}
+        t0 = time.perf_counter()
+        step(ev, warm=None)
+        torch.cuda.synchronize()
+        times.append((time.perf_counter() - t0) * 1e3)
+        evs.append(ev)
+        log(f"step {i}: {times[-1]:.2f} ms")
+    return np.array(times), evs
+
+
+def E():
+    return torch.cuda.Event(enable_timing=True)
+
+
+# ---------------------------------------------------------------------------
+# 7B-shaped ragged batch: one compression, then 256 decode calls
+# ---------------------------------------------------------------------------
+
+def run_batch(args, wl, dev):
+    ci = I.make_cache(wl, device=dev)                           # the pristine cache
+    NL, Bsz, H, Cap, D = ci.k.shape
+    e, Hq, w = wl.elem_bytes, wl.n_q_heads, wl.window
+    log(f"generated pristine cache {tuple(ci.k.shape)}, lengths {int(ci.seq_len.min())}-{int(ci.seq_len.max())}")
+    kw, vw, lw = torch.empty_like(ci.k), torch.empty_like(ci.v), torch.empty_like(ci.length)
+    cache = B.KVCache(kw, vw, lw)
+    retention = torch.tensor([B.reco_retention_from_reward(float(v)) for v in ci.reward], dtype=torch.float64,
+                             device=dev)
+    qs, ks, vs = I.make_decode_inputs(wl, ci, wl.decode_steps, device=dev)
+    scores = torch.zeros((NL, Bsz, H, Cap), dtype=torch.float32, device=dev)
+    kept = torch.zeros((NL, Bsz, H, Cap), dtype=torch.int32, device=dev)
+    ws_score = torch.empty(B.score_workspace_size(cache, Hq, w), dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(B.select_compact_workspace_size(cache), dtype=torch.uint8, device=dev)
+    ws_dec = B.decode_workspace(cache, Hq)
+    out = torch.empty_like(qs[0])
+    lse = torch.empty((NL, Bsz, Hq), dtype=torch.float32, device=dev)
+    dev_err = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def restore():
+        kw.copy_(ci.k)
+        vw.copy_(ci.v)
+        lw.copy_(ci.length)
+
+    def step(ev, warm):
+        rec = (lambda k: ev.setdefault(k, E()).record()) if ev is not None else (lambda k: None)
+        rec("c0")
+        B.reco_score(cache, ci.q_win, w, scores=scores, ws=ws_score, dev_err=dev_err)
+        rec("c1")
+        B.reco_select_compact(cache, scores, retention, w, kept_idx=kept, ws=ws_sel, dev_err=dev_err)
+        rec("c2")
+        for s in range(wl.decode_steps):
+            B.reco_decode_attn(cache, qs[s], ks[s], vs[s], out=out, lse=lse, ws=ws_dec, dev_err=dev_err)
+        rec("d1")
+
+    times, evs = timed_steps(args, restore, step)
+    if dev_err.item() != 0:
+        raise RuntimeError(f"device error {dev_err.item()}")
+    lens0 = ci.length.cpu().numpy().astype(np.int64)
+    m = lw.cpu().numpy().astype(np.int64) - wl.decode_steps
+    moved = moved_rows_of(kept, m)
+    cb = compress_bytes(lens0, m, moved, Bsz, Hq, w, D, e)
+    dec = [decode_call_bytes(int((m + s + 1).sum()), m.size, NL * Bsz * Hq, D, e) for s in range(wl.decode_steps)]
+    step_bytes = sum(cb.values()) + sum(dec)
+    comp_tok = NL * int(ci.seq_len.sum())
+    dec_tok = sum(NL * int((m[0, :, 0] + s + 1).sum()) for s in range(wl.decode_steps))
+    ms = float(times.mean())
+    dec_ms = np.array([ev["c2"].elapsed_time(ev["d1"]) for ev in evs]) / wl.decode_steps
+    extra = {
+        "kv_tokens_per_step": {"compress": comp_tok, "decode": dec_tok},
+        "compress_algorithmic_bytes": dict(cb, compact_moved_rows=moved),
+        "phase_ms": {"score": float(np.mean([ev["c0"].elapsed_time(ev["c1"]) for ev in evs])),
+                     "select_compact": float(np.mean([ev["c1"].elapsed_time(ev["c2"]) for ev in evs])),
+                     "decode_call": float(dec_ms.mean()),
+                     "decode_calls_total": float(np.mean([ev["c2"].elapsed_time(ev["d1"]) for ev in evs]))},
+        "roofline": roofline_obj(DECODE_KERNELS, float(np.mean(dec)), float(dec_ms.mean())),
+    }
+    if args.cpu_baseline:
+        log("timing the CPU oracle on sampled units")
+        scale = 1.0 / math.sqrt(D)
+        rng = np.random.default_rng(wl.seed)
+        r_seq = [oracle_retention(float(v)) for v in ci.reward]
+        order = [tuple(int(x) for x in np.unravel_index(i, (NL, Bsz, H))) for i in rng.permutation(NL * Bsz * H)]
+        G = wl.group
+
+        def comp_samples():
+            for u in order:
+                L = int(lens0[u])
+                yield (I.to_f64(ci.k[u][:L]), I.to_f64(ci.v[u][:L]),
+                       I.to_f64(ci.q_win[u[0], u[1], u[2] * G:(u[2] + 1) * G]), r_seq[u[1]])
+
+        def dec_samples():
+            for j, u in enumerate(order):
+                s_idx = (j * 37) % wl.decode_steps
+                n = int(m[u]) + s_idx
+                K = I.to_f64(ci.k[u][:n])
+                yield (K, I.to_f64(ci.v[u][:n]), n, I.to_f64(qs[s_idx][u[0], u[1], u[2] * G:(u[2] + 1) * G]),
+                       I.to_f64(ks[s_idx][u]), I.to_f64(vs[s_idx][u]))
+        threads, affinity = host_threads()
+        from threadpoolctl import threadpool_limits, threadpool_info
+        with threadpool_limits(limits=threads):
+            cores = max([p_.get("num_threads", 1) for p_ in threadpool_info()] + [1])
+            rt = oracle_unit_rates(comp_samples(), dec_samples(), scale, w, 8.0, 10.0)
+        rows_comp = NL * H * int(ci.seq_len.sum())
+        rows_dec = sum(int((m + s + 1).sum()) for s in range(wl.decode_steps))
+        est = rt["s_per_row_compress"] * rows_comp + rt["s_per_row_decode"] * rows_dec
+        extra["cpu_baseline"] = {
+            "value": (comp_tok + dec_tok) / est, "unit": "KV tokens/s", "cores": int(cores),
+            "affinity_cores": affinity, "avg_busy_threads": round(rt["busy"], 2), "kind": "oracle",
+            "sample": (f"{rt['units_compressed']} whole units compressed ({rt['t_compress']:.1f} s) and "
+                       f"{rt['decode_samples']} single-unit decode calls spread over the 256-call range "
+                       f"({rt['t_decode']:.1f} s); per-row oracle costs of each phase scaled to the step's "
+                       f"{rows_comp} scored and {rows_dec} attended unit rows (extrapolated, "
+                       f"{est:.0f} s estimated per step)")}
+    emit_line(args, wl, (comp_tok + dec_tok) / (ms * 1e-3), ms, step_bytes, extra,
+              {"batch": Bsz, "cache_len_min": int(ci.seq_len.min()), "cache_len_max": int(ci.seq_len.max()),
+               "decode_steps": wl.decode_steps, "kept_rows_total": int(m.sum())})
+
+
+def oracle_retention(v: float) -> float:
+    import oracle
+    return oracle.retention_from_reward(v)
+
+
+# ---------------------------------------------------------------------------
+# 32B-shaped batch: four rounds of (compression -> 64 decode calls)
+# ---------------------------------------------------------------------------
+
+ROUNDS_32B = 4
+
+
+def run_32b(args, wl, dev):
+    steps, w, G, V = wl.decode_steps, wl.window, wl.group, wl.vocab
+    cap = int(wl.lengths[0]) + ROUNDS_32B * steps
+    state = {"ci": None}
+
+    def regenerate():
+        if state["ci"] is not None:
+            state["ci"] = None
+            torch.cuda.empty_cache()
+        state["ci"] = I.make_cache(wl, device=dev, capacity=cap)
+        log("generated the cache from its seed (untimed)")
+
+    regenerate()
+    ci = state["ci"]
+    NL, Bsz, H, Cap, D = ci.k.shape
+    e, Hq = wl.elem_bytes, wl.n_q_heads
+    log(f"generated cache {tuple(ci.k.shape)} ({2 * ci.k.numel() * e / 1e9:.1f} GB)")
+    rewards = I.make_rewards("beta22", ROUNDS_32B, Bsz, seed=wl.seed + 31)
+    r_rounds = [[B.reco_retention_from_reward(float(v)) for v in rewards[k]] for k in range(ROUNDS_32B)]
+    ret = [torch.tensor(r, dtype=torch.float64, device=dev) for r in r_rounds]
+    dec_in = [I.make_decode_inputs(wl, ci, steps, seed_offset=k + 1, device=dev) for k in range(ROUNDS_32B)]
+    logits = [I.make_logits(steps * Bsz, V, seed=wl.seed + 17 + k, device=dev) for k in range(ROUNDS_32B)]
+    row_reward = [torch.from_numpy(rewards[k].astype(np.float32)).to(dev).repeat(steps).contiguous()
+                  for k in range(ROUNDS_32B)]
+    refl = torch.from_numpy(I.make_reflection_ids(N_REFL, V, seed=wl.seed + 19)).to(dev)
+    ans_logits = I.make_logits(Bsz * ANSWER_LEN, V, seed=wl.seed + 23, device=dev, shape=(Bsz, ANSWER_LEN, V))
+    ans_tok = torch.from_numpy(I.make_answer_tokens(Bsz, ANSWER_LEN, V, seed=wl.seed + 29)).to(dev)
+    scores = torch.zeros((NL, Bsz, H, Cap), dtype=torch.float32, device=dev)
+    kept = torch.zeros((NL, Bsz, H, Cap), dtype=torch.int32, device=dev)
+    probe_cache = B.KVCache(ci.k, ci.v, ci.length)
+    ws_score = torch.empty(B.score_workspace_size(probe_cache, Hq, w), dtype=torch.uint8, device=dev)
+    ws_sel = torch.empty(B.select_compact_workspace_size(probe_cache), dtype=torch.uint8, device=dev)
+    ws_dec = B.decode_workspace(probe_cache, Hq)
+    ws_smp = torch.empty(B.penalty_sample_workspace_size(steps * Bsz, V), dtype=torch.uint8, device=dev)
+    ws_ppl = torch.empty(B.answer_ppl_workspace_size(Bsz, ANSWER_LEN, V), dtype=torch.uint8, device=dev)
+    del probe_cache, ci
+    tokens = torch.empty(steps * Bsz, dtype=torch.int32, device=dev)
+    out = torch.empty((NL, Bsz, Hq, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((NL, Bsz, Hq), dtype=torch.float32, device=dev)
+    stats = torch.empty((steps, NL, Bsz, Hq, 2), dtype=torch.float32, device=dev)
+    ppl = torch.empty(Bsz, dtype=torch.float32, device=dev)
+    stop = torch.empty(Bsz, dtype=torch.int32, device=dev)
+    dev_err = torch.zeros(1, dtype=torch.int32, device=dev)
+    side = torch.cuda.Stream(device=dev)
+    acct = {"lens0": [], "m": [], "moved": []}
+
+    def step(ev, warm):
+        ci_ = state["ci"]
+        cache = B.KVCache(ci_.k, ci_.v, ci_.length)
+        main = torch.cuda.current_stream()
+        q_win, st = ci_.q_win, None
+        for k in range(ROUNDS_32B):
+            if warm == 0:
+                acct["lens0"].append(ci_.length.cpu().numpy().astype(np.int64))
+            if ev is not None:
+                ev.setdefault(f"c0_{k}", E()).record()
+            B.reco_score(cache, q_win, w, scores=scores, ws=ws_score, dev_err=dev_err, row_stats=st)
+            if ev is not None:
+                ev.setdefault(f"c1_{k}", E()).record()
+            B.reco_select_compact(cache, scores, ret[k], w, kept_idx=kept, ws=ws_sel, dev_err=dev_err)
+            if ev is not None:
+                ev.setdefault(f"c2_{k}", E()).record()
+            if warm == 0:
+                m_k = ci_.length.cpu().numpy().astype(np.int64)
+                acct["m"].append(m_k)
+                acct["moved"].append(moved_rows_of(kept, m_k))
+            side.wait_stream(main)
+            with torch.cuda.stream(side):
+                B.reco_penalty_sample(logits[k], refl, row_reward[k], TAU_LO, TAU_HI, *BETAS, TEMPERATURE,
+                                      SAMPLE_SEED, k, tokens=tokens, ws=ws_smp, dev_err=dev_err)
+            qs, ks, vs = dec_in[k]
+            for s in range(steps):
+                B.reco_decode_attn(cache, qs[s], ks[s], vs[s], out=out, lse=lse, ws=ws_dec, dev_err=dev_err,
+                                   row_stats=stats[s])
+            if ev is not None:
+                ev.setdefault(f"d1_{k}", E()).record()
+            main.wait_stream(side)
+            # the next round's window: the last w decode queries and their statistics
+            q_win = torch.stack(qs[-w:], dim=3).contiguous()
+            st = stats[-w:].permute(1, 2, 3, 0, 4).contiguous()
+        if ev is not None:
+            ev.setdefault("p0", E()).record()
+        B.reco_answer_ppl(ans_logits, ans_tok, TAU_P, ppl=ppl, stop=stop, ws=ws_ppl, dev_err=dev_err)
+        if ev is not None:
+            ev.setdefault("p1", E()).record()
+
+    first = {"done": False}
+
+    def restore():
+        if first["done"]:
+            regenerate()
+        first["done"] = True
+
+    times, evs = timed_steps(args, restore, step)
+    if dev_err.item() != 0:
+        raise RuntimeError(f"device error {dev_err.item()}")
+    step_bytes = 0
+    comp_tok = dec_tok = 0
+    round_info, dec_bytes_all = [], []
+    for k in range(ROUNDS_32B):
+        lens0, m, moved = acct["lens0"][k], acct["m"][k], acct["moved"][k]
+        cb = compress_bytes(lens0, m, moved, Bsz, Hq, w, D, e, stats_fed=k > 0)
+        dec = [decode_call_bytes(int((m + s + 1).sum()), m.size, NL * Bsz * Hq, D, e) for s in range(steps)]
+        dec_bytes_all += dec
+        step_bytes += sum(cb.values()) + sum(dec) + steps * Bsz * (V * 4 + N_REFL * 4 + 4)
+        comp_tok += NL * int(lens0[:, :, 0].sum())
+        dec_tok += sum(NL * int((m[0, :, 0] + s + 1).sum()) for s in range(steps))
+        round_info.append({"scoring": "two-pass" if k == 0 else "one-pass (decode statistics)",
+                           "rows_scored": int(lens0.sum()), "kept_rows": int(m.sum()), "moved_rows": moved,
+                           "score_ms": float(np.mean([ev[f"c0_{k}"].elapsed_time(ev[f"c1_{k}"]) for ev in evs])),
+                           "select_compact_ms": float(np.mean([ev[f"c1_{k}"].elapsed_time(ev[f"c2_{k}"])
+                                                               for ev in evs])),
+                           "decode_call_ms": float(np.mean([ev[f"c2_{k}"].elapsed_time(ev[f"d1_{k}"])
+                                                            for ev in evs])) / steps,
+                           "score_K_TBps": int(lens0.sum()) * D * e / 1e12 /
+                           (np.mean([ev[f"c0_{k}"].elapsed_time(ev[f"c1_{k}"]) for ev in evs]) * 1e-3)})
+    step_bytes += Bsz * ANSWER_LEN * V * 4
+    ms = float(times.mean())
+    dec_ms_total = sum(r["decode_call_ms"] * steps for r in round_info)
+    dec_avg_ms = dec_ms_total / (steps * ROUNDS_32B)
+    extra = {
+        "kv_tokens_per_step": {"compress": comp_tok, "decode": dec_tok},
+        "rounds": round_info,
+        "phase_ms": {"answer_ppl": float(np.mean([ev["p0"].elapsed_time(ev["p1"]) for ev in evs])),
+                     "decode_call": dec_avg_ms},
+        "roofline": roofline_obj(DECODE_KERNELS, float(np.mean(dec_bytes_all)), dec_avg_ms),
+    }
+    if args.cpu_baseline:
+        log("timing the CPU oracle on sampled units")
+        regenerate()                  # a fresh regeneration: the pre-compression cache
+        ci_ = state["ci"]
+        scale = 1.0 / math.sqrt(D)
+        rng = np.random.default_rng(wl.seed)
+        order = [tuple(int(x) for x in np.unravel_index(i, (NL, Bsz, H))) for i in rng.permutation(NL * Bsz * H)]
+        m1 = acct["m"][0]
+        qs0, ks0, vs0 = dec_in[0]
+
+        def comp_samples():
+            for u in order:
+                L = int(ci_.length[u].item())
+                yield (I.to_f64(ci_.k[u][:L]), I.to_f64(ci_.v[u][:L]),
+                       I.to_f64(ci_.q_win[u[0], u[1], u[2] * G:(u[2] + 1) * G]), r_rounds[0][u[1]])
+
+        def dec_samples():
+            for j, u in enumerate(order):
+                s_idx = (j * 37) % steps
+                n = int(m1[u]) + s_idx
+                yield (I.to_f64(ci_.k[u][:n]), I.to_f64(ci_.v[u][:n]), n,
+                       I.to_f64(qs0[s_idx][u[0], u[1], u[2] * G:(u[2] + 1) * G]), I.to_f64(ks0[s_idx][u]),
+                       I.to_f64(vs0[s_idx][u]))
+        threads, affinity = host_threads()
+        from threadpoolctl import threadpool_limits, threadpool_info
+        with threadpool_limits(limits=threads):
+            cores = max([p_.get("num_threads", 1) for p_ in threadpool_info()] + [1])
+            rt = oracle_unit_rates(comp_samples(), dec_samples(), scale, w, 10.0, 10.0)
+        rows_comp = sum(int(acct["lens0"][k].sum()) for k in range(ROUNDS_32B))
+        rows_dec = sum(int((acct["m"][k] + s + 1).sum()) for k in range(ROUNDS_32B) for s in range(steps))
+        est = rt["s_per_row_compress"] * rows_comp + rt["s_per_row_decode"] * rows_dec
+        extra["cpu_baseline"] = {
+            "value": (comp_tok + dec_tok) / est, "unit": "KV tokens/s", "cores": int(cores),
+            "affinity_cores": affinity, "avg_busy_threads": round(rt["busy"], 2), "kind": "oracle",
+            "sample": (f"{rt['units_compressed']} whole 65,536-row units compressed ({rt['t_compress']:.1f} s) and "
+                       f"{rt['decode_samples']} single-unit decode calls of round 1 ({rt['t_decode']:.1f} s); "
+                       f"per-row oracle costs of each phase scaled to the step's {rows_comp} scored and "
+                       f"{rows_dec} attended unit rows over the four rounds (extrapolated, {est:.0f} s "
+                       f"estimated per step)")}
+    emit_line(args, wl, (comp_tok + dec_tok) / (ms * 1e-3), ms, step_bytes, extra,
+              {"batch": Bsz, "cache_len": int(wl.lengths[0]), "rounds": ROUNDS_32B, "decode_steps_per_round": steps,
+               "vocab": V, "answer_len": ANSWER_LEN})
+
+
+# ---------------------------------------------------------------------------
+# 8B-shaped trajectory through the controller
+# ---------------------------------------------------------------------------
+
+TRAJ_CAP = 8192
+
+
+def run_trajectory(args, wl, dev):
+    from paper_2608_04771_amd.controller import RecoDecoder, RecoPolicy
+    T, w, V = wl.decode_steps, wl.window, wl.vocab
+    ci = I.make_cache(wl, device=dev, capacity=TRAJ_CAP)
+    NL, Bsz, H, Cap, D = ci.k.shape
+    e, Hq = wl.elem_bytes, wl.n_q_heads
+    prompt = int(ci.seq_len[0])
+    k0, v0, l0 = ci.k[..., :prompt, :].clone(), ci.v[..., :prompt, :].clone(), ci.length.clone()
+    steps_len = I.make_step_lengths(T, 200, wl.seed)
+    bounds = set(int(x) for x in np.cumsum(steps_len))
+    rewards = I.make_rewards("beta25", len(steps_len), Bsz, wl.seed + 1)
+    refl = torch.from_numpy(I.make_reflection_ids(wl.n_reflection_ids, V, seed=wl.seed + 19)).to(dev)
+    pol = RecoPolicy(retention="clamp", window=w, interval=0)
+    # every token's inputs, resident in HBM before the timed region
+    qa = torch.empty((T, NL, Bsz, Hq, D), dtype=torch.bfloat16, device=dev)
+    ka = torch.empty((T, NL, Bsz, H, D), dtype=torch.bfloat16, device=dev)
+    va = torch.empty_like(ka)
+    za = torch.empty((T, Bsz, V), dtype=torch.float32, device=dev)
+    for t0 in range(0, T, 1024):
+        n = min(1024, T - t0)
+        qs, ks, vs = I.make_decode_inputs(wl, ci, n, seed_offset=t0, device=dev)
+        qa[t0:t0 + n] = torch.stack(qs)
+        ka[t0:t0 + n] = torch.stack(ks)
+        va[t0:t0 + n] = torch.stack(vs)
+        za[t0:t0 + n] = I.make_logits(n * Bsz, V, seed=wl.seed + 100 + t0, device=dev).view(n, Bsz, V)
+    log(f"staged the inputs of {T} tokens ({(qa.numel() + ka.numel() * 2) * 2 / 1e9 + za.numel() * 4 / 1e9:.1f} GB)")
+    state = {}
+    sample_every = 64
+    acct = {"comp_rows": [], "m": [], "moved": [], "dec_rows": [], "fed": 0}
+
+    def restore():
+        ci.k[..., :prompt, :] = k0
+        ci.v[..., :prompt, :] = v0
+        ci.length.copy_(l0)
+        state["dec"] = RecoDecoder(B.KVCache(ci.k, ci.v, ci.length), Hq, pol, ci.q_win, refl,
+                                   record_kept=True)
+
+    def step(ev, warm):
+        dec = state["dec"]
+        bi = 0
+        for t in range(T):
+            slot = dec.query_slot()
+            slot.copy_(qa[t])
+            timed = ev is not None and t % sample_every == 0
+            if timed:
+                ev.setdefault(f"a{t}", E()).record()
+            dec.decode(slot, ka[t], va[t])
+            if timed:
+                ev.setdefault(f"b{t}", E()).record()
+            if warm == 0:
+                acct["dec_rows"].append(dec.lengths()[0])
+            dec.sample(za[t], temperature=TEMPERATURE, seed=SAMPLE_SEED)
+            if t + 1 in bounds:
+                L_before = dec.lengths()[0]
+                done, _ = dec.end_step([float(x) for x in rewards[bi]])
+                bi += 1
+                if warm == 0 and done:
+                    m_now = dec.lengths()[0]
+                    acct["comp_rows"].append(L_before)
+                    acct["m"].append(m_now)
+                    acct["fed"] += int(dec.last_score_stats_fed)
+                    mm = np.full((NL, Bsz, H), m_now, dtype=np.int64)
+                    acct["moved"].append(moved_rows_of(dec.kept, mm))
+
+    times, evs = timed_steps(args, restore, step)
+    if state["dec"].dev_err.item() != 0:
+        raise RuntimeError(f"device error {state['dec'].dev_err.item()}")
+    units = NL * Bsz * H
+    comp_tok = NL * Bsz * int(np.sum(acct["comp_rows"]))
+    dec_tok = NL * Bsz * int(np.sum(acct["dec_rows"]))          # rows attended per call (the new one included)
+    step_bytes = 0
+    for Lb, m_, mv in zip(acct["comp_rows"], acct["m"], acct["moved"]):
+        cb = compress_bytes(np.full((NL, Bsz, H), Lb), np.full((NL, Bsz, H), m_), mv, Bsz, Hq, w, D, e)
+        step_bytes += sum(cb.values())
+    dec_bytes = [decode_call_bytes(n * units, units, NL * Bsz * Hq, D, e) for n in acct["dec_rows"]]
+    step_bytes += sum(dec_bytes) + T * Bsz * (V * 4 + wl.n_reflection_ids * 4 + 4)
+    samp = [t for t in range(0, T, sample_every)]
+    dec_ms = np.array([[ev[f"a{t}"].elapsed_time(ev[f"b{t}"]) for t in samp] for ev in evs]).mean(axis=0)
+    samp_bytes = np.array([dec_bytes[t] for t in samp])
+    ms = float(times.mean())
+    extra = {
+        "kv_tokens_per_step": {"compress": comp_tok, "decode": dec_tok},
+        "trajectory": {"generated_tokens": T, "prompt": prompt, "reasoning_steps": len(steps_len),
+                       "compressions": len(acct["comp_rows"]), "one_pass_scores": acct["fed"],
+                       "mean_rows_attended_per_unit": float(np.mean(acct["dec_rows"])),
+                       "us_per_token": ms * 1e3 / T},
+        "roofline": roofline_obj(DECODE_KERNELS + ", every 64th call of the trajectory timed",
+                                 float(samp_bytes.mean()), float(dec_ms.mean())),
+    }
+    if args.cpu_baseline:
+        log("timing the CPU oracle on the start of the trajectory")
+        extra["cpu_baseline"] = cpu_baseline_trajectory(wl, ci, k0, v0, prompt, qa, ka, va, bounds, rewards, w)
+    emit_line(args, wl, (comp_tok + dec_tok) / (ms * 1e-3), ms, step_bytes, extra,
+              {"batch": Bsz, "prompt": prompt, "generated_tokens": T, "mean_step_len": 200, "vocab": V,
+               "capacity": TRAJ_CAP})
+
+
+def cpu_baseline_trajectory(wl, ci, k0, v0, prompt, qa, ka, va, bounds, rewards, w, budget_s: float = 12.0):
+    """The oracle runs the trajectory from the prompt (decode with append on
+    every token, Eq. 2 compression of every unit at each step boundary) until
+    its time budget is used; the rate is the KV tokens it processed over the
+    time it took."""
+    import oracle
+    from threadpoolctl import threadpool_limits, threadpool_info
+    NL, Bsz, H, _, D = ci.k.shape
+    Hq = wl.n_q_heads
+    scale = 1.0 / math.sqrt(D)
+    cap = prompt + 4096
+    K = np.zeros((NL, Bsz, H, cap, D))
+    V = np.zeros_like(K)
+    K[..., :prompt, :] = I.to_f64(k0)
+    V[..., :prompt, :] = I.to_f64(v0)
+    lens = np.full((NL, Bsz, H), prompt, dtype=np.int64)
+    ring = list(np.moveaxis(I.to_f64(ci.q_win), 3, 0))        # the last w queries, oldest first
+    threads, affinity = host_threads()
+    tok = comp = dec = 0
+    t_used = cpu = 0.0
+    bi = 0
+    with threadpool_limits(limits=threads):
+        cores = max([p_.get("num_threads", 1) for p_ in threadpool_info()] + [1])
+        while t_used < budget_s and tok < min(4096, qa.shape[0]):
+            q, kn, vn = I.to_f64(qa[tok]), I.to_f64(ka[tok]), I.to_f64(va[tok])
+            c0, t0 = time.process_time(), time.perf_counter()
+            oracle.decode_cache(K, V, lens, q, scale, kn, vn)
+            dec += NL * Bsz * int(lens[0, 0, 0])
+            ring = ring[1:] + [q]
+            tok += 1
+            if tok in bounds:
+                r = [oracle.retention_from_reward(float(v)) for v in rewards[bi]]
+                bi += 1
+                comp += NL * Bsz * int(lens[0, 0, 0])
+                _, _, K, V, lens = oracle.compress_cache(K, V, lens, np.stack(ring, axis=3), r, w, scale)
+            t_used += time.perf_counter() - t0
+            cpu += time.process_time() - c0
+    return {"value": (comp + dec) / t_used, "unit": "KV tokens/s", "cores": int(cores), "affinity_cores": affinity,
+            "avg_busy_threads": round(cpu / max(t_used, 1e-9), 2), "kind": "oracle",
+            "sample": (f"the first {tok} generated tokens of the trajectory ({bi} compressions, {t_used:.1f} s): "
+                       f"decode with append on all {NL * Bsz * H} units per token and Eq. 2 compression of "
+                       f"every unit at each step boundary; the rate is the KV tokens processed over that time")}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    # The batch, 32B and trajectory workloads do not fit this bench's one
-    # pristine cache copy per step; the full-size GPU tests measure them.
-    ap.add_argument("--workload", default="7b16k", choices=["7b16k", "tiny"])
+    ap.add_argument("--workload", default="7b16k", choices=["7b16k", "tiny", "7b-batch32", "32b64k",
+                                                             "8b-trajectory"])
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
     ap.add_argument("--no-extras", dest="extras", action="store_false",
                     help="skip the measurements made after the timed steps (for profiler runs)")
@@ -371,6 +956,10 @@ def main():
     dev = torch.device("cuda:0")
     B.load_library()
     wl = I.WORKLOADS[args.workload]
+    runner = {"7b-batch32": run_batch, "32b64k": run_32b, "8b-trajectory": run_trajectory}.get(args.workload)
+    if runner is not None:
+        runner(args, wl, dev)
+        return
     copies = args.warmup + args.steps
     w = Workload(wl, copies, dev)
     torch.cuda.synchronize()

@@ -64,9 +64,9 @@ ANSWER_LEN = 32
 DECODE_TRAFFIC = {
     "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
                 "paper_2608_04771_amd/csrc/decode_attn.hpp"),
-    "sha256": "c32943c7a959a935db735c184a74d62495d0a4c6a6f2b30369b0685d872f471f",
+    "sha256": "5f11d3213882958644385b9b520ac593bd8b062a3bef62476ef01de9dfaf119a",
     "workload": "7b-28L-28q4kv-d128-bf16-L16384",
-    "fetch_bytes": 555477303,
+    "fetch_bytes": 555540033,
     "write_bytes": 817152,
 }
 
@@ -241,8 +241,15 @@ def decode_per_layer_graph(w: Workload, i: int, reps: int = 20):
         g.replay()
     e1.record()
     torch.cuda.synchronize()
-    return {"us_per_decode_step": e0.elapsed_time(e1) * 1e3 / reps, "calls_per_step": NL,
-            "cache_rows": int(cache.length.max().item())}
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    # rows attended per step, averaged over the timed replays (each appends one row per unit)
+    lens = cache.length.to(torch.int64)
+    rows = int(lens.sum().item()) - lens.numel() * (reps - 1) // 2
+    Hq, D, e = wl.n_q_heads, wl.head_dim, wl.elem_bytes
+    step_bytes = decode_call_bytes(rows, lens.numel(), NL * w.shape[1] * Hq, D, e)
+    gbps = step_bytes / (us * 1e-6) / 1e9
+    return {"us_per_decode_step": us, "calls_per_step": NL, "cache_rows": int(cache.length.max().item()),
+            "algorithmic_bytes_per_step": step_bytes, "achieved_GBps": gbps, "frac_of_peak_hbm": gbps / PEAK_HBM_GBPS}
 
 
 def copy_bandwidth(w: Workload):
@@ -790,6 +797,7 @@ def run_32b(args, wl, dev):
 # ---------------------------------------------------------------------------
 
 TRAJ_CAP = 8192
+PROBE_REPEATS = 8
 
 
 def run_trajectory(args, wl, dev):
@@ -829,18 +837,15 @@ def run_trajectory(args, wl, dev):
         state["dec"] = RecoDecoder(B.KVCache(ci.k, ci.v, ci.length), Hq, pol, ci.q_win, refl,
                                    record_kept=True)
 
-    def step(ev, warm):
+    def step(ev, warm, probe=None):
         dec = state["dec"]
         bi = 0
         for t in range(T):
             slot = dec.query_slot()
             slot.copy_(qa[t])
-            timed = ev is not None and t % sample_every == 0
-            if timed:
-                ev.setdefault(f"a{t}", E()).record()
             dec.decode(slot, ka[t], va[t])
-            if timed:
-                ev.setdefault(f"b{t}", E()).record()
+            if probe is not None and t % sample_every == 0:
+                probe_burst(dec, slot, probe)
             if warm == 0:
                 acct["dec_rows"].append(dec.lengths()[0])
             dec.sample(za[t], temperature=TEMPERATURE, seed=SAMPLE_SEED)
@@ -856,10 +861,43 @@ def run_trajectory(args, wl, dev):
                     mm = np.full((NL, Bsz, H), m_now, dtype=np.int64)
                     acct["moved"].append(moved_rows_of(dec.kept, mm))
 
+    def probe_burst(dec, slot, probe):
+        # The call just made, repeated back to back without the append (same
+        # rows, same sizes): a lead-in call, then PROBE_REPEATS calls between
+        # two events, so the events bracket decode kernels only.
+        cache = dec.cache
+        B.reco_decode_attn(cache, slot, out=probe["out"], lse=probe["lse"], ws=dec.ws_dec, dev_err=dec.dev_err)
+        a, b = E(), E()
+        a.record()
+        for _ in range(PROBE_REPEATS):
+            B.reco_decode_attn(cache, slot, out=probe["out"], lse=probe["lse"], ws=dec.ws_dec, dev_err=dec.dev_err)
+        b.record()
+        probe["ev"].append((a, b))
+        probe["rows"].append(dec.lengths()[0])
+
     times, evs = timed_steps(args, restore, step)
     if state["dec"].dev_err.item() != 0:
         raise RuntimeError(f"device error {state['dec'].dev_err.item()}")
     units = NL * Bsz * H
+    roof = None
+    if args.extras:
+        log("timing sampled decode calls of the trajectory back to back (untimed pass)")
+        probe = {"ev": [], "rows": [], "out": torch.empty((NL, Bsz, Hq, D), dtype=torch.bfloat16, device=dev),
+                 "lse": torch.empty((NL, Bsz, Hq), dtype=torch.float32, device=dev)}
+        restore()
+        torch.cuda.synchronize()
+        step(None, None, probe)
+        torch.cuda.synchronize()
+        if state["dec"].dev_err.item() != 0:
+            raise RuntimeError(f"device error {state['dec'].dev_err.item()}")
+        p_ms = np.array([a.elapsed_time(b) for a, b in probe["ev"]]) / PROBE_REPEATS
+        # rows attended per probe call: the cached rows (the append of the
+        # sampled call included), no new row
+        p_bytes = np.array([n * units * 2 * D * e + 2 * NL * Bsz * Hq * D * e + NL * Bsz * Hq * 4
+                            for n in probe["rows"]])
+        roof = roofline_obj(DECODE_KERNELS + f"; every {sample_every}th call of the trajectory repeated "
+                            f"{PROBE_REPEATS}x back to back without its append, after the timed steps",
+                            float(p_bytes.mean()), float(p_ms.mean()))
     comp_tok = NL * Bsz * int(np.sum(acct["comp_rows"]))
     dec_tok = NL * Bsz * int(np.sum(acct["dec_rows"]))          # rows attended per call (the new one included)
     step_bytes = 0
@@ -868,9 +906,6 @@ def run_trajectory(args, wl, dev):
         step_bytes += sum(cb.values())
     dec_bytes = [decode_call_bytes(n * units, units, NL * Bsz * Hq, D, e) for n in acct["dec_rows"]]
     step_bytes += sum(dec_bytes) + T * Bsz * (V * 4 + wl.n_reflection_ids * 4 + 4)
-    samp = [t for t in range(0, T, sample_every)]
-    dec_ms = np.array([[ev[f"a{t}"].elapsed_time(ev[f"b{t}"]) for t in samp] for ev in evs]).mean(axis=0)
-    samp_bytes = np.array([dec_bytes[t] for t in samp])
     ms = float(times.mean())
     extra = {
         "kv_tokens_per_step": {"compress": comp_tok, "decode": dec_tok},
@@ -878,8 +913,7 @@ def run_trajectory(args, wl, dev):
                        "compressions": len(acct["comp_rows"]), "one_pass_scores": acct["fed"],
                        "mean_rows_attended_per_unit": float(np.mean(acct["dec_rows"])),
                        "us_per_token": ms * 1e3 / T},
-        "roofline": roofline_obj(DECODE_KERNELS + ", every 64th call of the trajectory timed",
-                                 float(samp_bytes.mean()), float(dec_ms.mean())),
+        "roofline": roof,
     }
     if args.cpu_baseline:
         log("timing the CPU oracle on the start of the trajectory")

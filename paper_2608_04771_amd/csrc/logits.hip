@@ -197,8 +197,10 @@ constexpr int kPplThreads = 256;
 constexpr int kPplChunk = 16384;   // logits per workgroup
 
 // Per (row, chunk): the chunk's max and sum of exp(z - max), natural log domain.
-// Each thread holds its 64 logits of the chunk in registers (all requested in
-// one round trip), so the max and the sum need a single read of the chunk.
+// Each thread holds its logits of the chunk in registers (all requested in
+// one round trip, as 16-byte non-temporal loads where the rows allow), so
+// the max and the sum need a single read of the chunk.
+template <bool VEC>
 __global__ __launch_bounds__(kPplThreads) void ppl_partial_kernel(const float *logits, int vocab, int chunks,
                                                                   float *part) {
   constexpr int kPer = kPplChunk / kPplThreads;
@@ -212,10 +214,22 @@ __global__ __launch_bounds__(kPplThreads) void ppl_partial_kernel(const float *l
   const int wave = threadIdx.x / kWave;
 
   float x[kPer];
+  if constexpr (VEC) {
 #pragma unroll
-  for (int i = 0; i < kPer; ++i) {
-    const int j = c0 + i * kPplThreads + static_cast<int>(threadIdx.x);
-    x[i] = j < c1 ? z[j] : -INFINITY;
+    for (int i = 0; i < kPer / 4; ++i) {
+      const int j = c0 + (i * kPplThreads + static_cast<int>(threadIdx.x)) * 4;   // c1 - j is a multiple of 4
+      const uint4 u = j < c1 ? nt_load_u4(z + j) : make_uint4(0xff800000u, 0xff800000u, 0xff800000u, 0xff800000u);
+      x[4 * i + 0] = __uint_as_float(u.x);
+      x[4 * i + 1] = __uint_as_float(u.y);
+      x[4 * i + 2] = __uint_as_float(u.z);
+      x[4 * i + 3] = __uint_as_float(u.w);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int j = c0 + i * kPplThreads + static_cast<int>(threadIdx.x);
+      x[i] = j < c1 ? z[j] : -INFINITY;
+    }
   }
   float m = -INFINITY;
 #pragma unroll
@@ -327,8 +341,13 @@ hipError_t launch_answer_ppl(const float *logits, const int32_t *tokens, int bat
                              float *ppl, int32_t *stop, void *ws, int32_t *dev_err, hipStream_t s) {
   const int chunks = static_cast<int>((static_cast<int64_t>(vocab) + kPplChunk - 1) / kPplChunk);
   float *part = reinterpret_cast<float *>(ws);
-  hipLaunchKernelGGL(ppl_partial_kernel, dim3(chunks, batch * n), dim3(kPplThreads), 0, s, logits, vocab, chunks,
-                     part);
+  const bool vec = vocab % 4 == 0 && reinterpret_cast<uintptr_t>(logits) % 16 == 0;
+  if (vec)
+    hipLaunchKernelGGL(ppl_partial_kernel<true>, dim3(chunks, batch * n), dim3(kPplThreads), 0, s, logits, vocab,
+                       chunks, part);
+  else
+    hipLaunchKernelGGL(ppl_partial_kernel<false>, dim3(chunks, batch * n), dim3(kPplThreads), 0, s, logits, vocab,
+                       chunks, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(ppl_final_kernel, dim3(batch), dim3(kPplThreads), 0, s, logits, tokens, n, vocab, chunks, part,

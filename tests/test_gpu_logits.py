@@ -59,7 +59,7 @@ def _ppl_case(Bsz, n, vocab, seed, boost=None):
 
 
 @pytest.mark.parametrize("Bsz,n,vocab,boost", [(8, 32, 152064, (0, 3)), (2, 5, 1000, None), (1, 1, 17, (0,)),
-                                               (3, 7, 16385, (1,))])
+                                               (3, 7, 16385, (1,)), (2, 4, 128256, None), (1, 2, 16388, (0,))])
 def test_answer_ppl_matches_oracle(Bsz, n, vocab, boost):
     logits, tok = _ppl_case(Bsz, n, vocab, seed=vocab + n, boost=boost)
     dev_err = torch.zeros(1, dtype=torch.int32, device="cuda")
@@ -75,6 +75,22 @@ def test_answer_ppl_matches_oracle(Bsz, n, vocab, boost):
             assert bool(stop[b].item()) == bool(rstop[b])
     if boost:
         assert all(stop[b].item() == 1 for b in boost)
+
+
+def test_answer_ppl_unaligned_rows_match_oracle():
+    # a contiguous logits tensor whose base is 4 bytes past a 16-byte boundary
+    # (vocab a multiple of 4): the partial kernel takes its scalar-load path
+    Bsz, n, vocab = 2, 3, 4096
+    logits, tok = _ppl_case(Bsz, n, vocab, seed=11, boost=(1,))
+    flat = torch.empty(1 + Bsz * n * vocab, dtype=torch.float32, device="cuda")
+    z = flat[1:].view(Bsz, n, vocab)
+    z.copy_(logits.cuda())
+    assert z.data_ptr() % 16 == 4
+    ppl, _ = B.reco_answer_ppl(z, torch.from_numpy(tok).cuda(), 1.1)
+    torch.cuda.synchronize()
+    ref, _ = oracle.answer_ppl(logits.numpy(), tok, 1.1)
+    err = np.abs(np.log(ppl.cpu().numpy().astype(np.float64)) - np.log(ref))
+    assert err.max() <= 1e-5, err.max()
 
 
 def test_answer_ppl_uniform_logits_is_vocab():

@@ -63,10 +63,11 @@ ANSWER_LEN = 32
 # files change, the figure is reported as null until it is measured again.
 DECODE_TRAFFIC = {
     "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
-                "paper_2608_04771_amd/csrc/decode_attn.hpp"),
-    "sha256": "5f11d3213882958644385b9b520ac593bd8b062a3bef62476ef01de9dfaf119a",
+                "paper_2608_04771_amd/csrc/decode_attn.hpp", "paper_2608_04771_amd/csrc/decode_plan.hpp",
+                "paper_2608_04771_amd/csrc/decode_plan.cpp"),
+    "sha256": "0008d22a9dc393ea618f5dbdd8db574166e361e4bcaa36d4c869909036853450",
     "workload": "7b-28L-28q4kv-d128-bf16-L16384",
-    "fetch_bytes": 555540033,
+    "fetch_bytes": 555278186,
     "write_bytes": 817152,
 }
 

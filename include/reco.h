@@ -216,11 +216,17 @@ reco_status_t reco_decode_attn(const reco_kv_cache_t *cache, int32_t layer0, int
  * allocates nothing and the caller passes only inputs and outputs.  Every call
  * on one device shares that array and the array keeps the last call's
  * contents (no call depends on them): calls that overlap on one device race,
- * so serialise them (one stream, or events).  Returns RECO_ERR_WORKSPACE if
- * the call would need more than 8 MiB of partials (a call needs at most
- * compute_units * (16 * head_dim + 32) * 4 bytes, 2.1 MB on a 256-CU MI355X),
- * and RECO_ERR_HIP if the array's device address cannot be looked up; the
- * device current at the call must be the one `stream` belongs to. */
+ * so serialise them (one stream, or events).  The work is split as in
+ * reco_decode_attn, so the results agree bit for bit, except for a call with
+ * more units (n_layers * batch * n_kv_heads) than the device has compute
+ * units whose two-way split would need more than the 8 MiB: it finalises each
+ * unit in one workgroup instead, and its results may then differ from
+ * reco_decode_attn's in the last bits (within the decode tolerances).
+ * Returns RECO_ERR_WORKSPACE if the call would still need more than 8 MiB of
+ * partials (with fewer units than compute units a call needs at most
+ * compute_units * (16 * head_dim + 32) * 4 bytes, 2.1 MB on a 256-CU
+ * MI355X), and RECO_ERR_HIP if the array's device address cannot be looked
+ * up; the device current at the call must be the one `stream` belongs to. */
 reco_status_t reco_decode_attn_noalloc(const reco_kv_cache_t *cache, int32_t layer0, int32_t n_layers,
                                        const void *q, int32_t n_q_heads, float scale, const void *k_new,
                                        const void *v_new, void *out, float *lse, float *row_stats,

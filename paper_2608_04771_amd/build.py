@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libreco.so")
 ARCH = "gfx950"
 
 HIP_SOURCES = ["decode_attn.hip", "score.hip", "select_compact.hip", "pool_scores.hip", "logits.hip"]
-HOST_SOURCES = ["abi.cpp"]
+HOST_SOURCES = ["abi.cpp", "decode_plan.cpp"]
 
 # Packed fp32 instructions are kept out of every kernel (v_pk_* fp32 forms).
 NO_PACKED_FP32 = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

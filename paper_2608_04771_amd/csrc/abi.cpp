@@ -290,7 +290,8 @@ reco_status_t decode_common(const reco_kv_cache_t *cache, int32_t layer0, int32_
   p.out = out;
   p.lse = lse;
   p.row_stats = row_stats;
-  p.splits = reco::decode_splits(units, cache->capacity, cus);
+  p.splits = use_scratch ? reco::decode_scratch_splits(units, cache->capacity, cache->head_dim, cus)
+                         : reco::decode_splits(units, cache->capacity, cus);
   p.part_o = reinterpret_cast<float *>(ws);
   p.part_ml = p.part_o + static_cast<size_t>(units) * p.splits * 16 * cache->head_dim;
   p.dev_err = dev_err;

@@ -24,6 +24,7 @@
 // workgroups depend on.
 #include "reco_device.hpp"
 #include "decode_attn.hpp"
+#include "decode_plan.hpp"
 
 #include <math.h>
 
@@ -34,10 +35,10 @@ namespace reco {
 
 namespace {
 
-constexpr int kTile = 32;        // keys per wave iteration
+constexpr int kTile = kDecodeTile;   // keys per wave iteration
 constexpr int kWavesPerWG = 4;
 constexpr int kThreads = kWavesPerWG * kWave;
-constexpr int kMaxSplits = 128;
+constexpr int kMaxSplits = kDecodeMaxSplits;
 
 template <typename T, int D>
 struct DecodeCfg {
@@ -603,33 +604,6 @@ hipError_t launch_typed(const DecodeParams &p, hipStream_t s) {
 }
 
 }  // namespace
-
-// Splits per unit: at most one workgroup per compute unit of the device
-// (256 on a whole MI355X, fewer on a partition of it).  Measured on the
-// 7B-shaped cache, a single resident round with one workgroup per CU streams
-// fastest: two workgroups sharing a CU finish later than the rest, and a
-// second round adds its ramp to the tail.  At least four 32-key tiles per
-// split at capacity.
-int decode_splits(int units, int capacity, int compute_units) {
-  const int tiles_cap = (capacity + 1 + kTile - 1) / kTile;
-  int splits = compute_units / units;
-  int max_splits = tiles_cap / 4;
-  if (max_splits > kMaxSplits) max_splits = kMaxSplits;
-  if (max_splits < 1) max_splits = 1;
-  if (splits > max_splits) splits = max_splits;
-  if (splits < 1) splits = 1;
-  return splits;
-}
-
-size_t decode_workspace_bytes(int units, int capacity, int head_dim, int compute_units) {
-  const size_t splits = static_cast<size_t>(decode_splits(units, capacity, compute_units));
-  return static_cast<size_t>(units) * splits * (16 * static_cast<size_t>(head_dim) + 32) * sizeof(float);
-}
-
-size_t decode_scratch_bytes(int units, int capacity, int head_dim, int compute_units) {
-  if (decode_splits(units, capacity, compute_units) == 1) return 0;   // finalised in place, no partials
-  return decode_workspace_bytes(units, capacity, head_dim, compute_units);
-}
 
 // Split partials of the allocation-free entry point.  Every device holds its
 // own copy of this array at its own address until the process ends.  In host

@@ -25,19 +25,11 @@ struct DecodeParams {
   int layer0, n_layers, batch, hkv, cap, group, hq, splits;
   float scale_log2;       // logit scale * log2(e)
 };
-// compute_units: CUs of the device the call runs on (sets the split count).
-int decode_splits(int units, int capacity, int compute_units);
-size_t decode_workspace_bytes(int units, int capacity, int head_dim, int compute_units);
 hipError_t launch_decode(const DecodeParams &p, int dtype, int head_dim, hipStream_t s);
 
 // ---- allocation-free decode: split partials in a file-scope device array ----
-// Size of that array on every device (the split partials of one call need at
-// most compute_units * (16 * head_dim + 32) * 4 bytes: 2.1 MB on a 256-CU
-// device at head_dim 128).
-constexpr size_t kDecodeScratchBytes = size_t(8) << 20;
-// Bytes of the array one call uses (0 when every unit is a single split,
-// which needs no partials).
-size_t decode_scratch_bytes(int units, int capacity, int head_dim, int compute_units);
+// (kDecodeScratchBytes on every device; see decode_plan.hpp for its size and
+// the split rule of such calls.)
 // Device address of the current device's array, looked up with
 // hipGetSymbolAddress on the first call per device and kept.
 hipError_t decode_scratch(void **ptr);

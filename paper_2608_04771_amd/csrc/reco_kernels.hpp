@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "decode_attn.hpp"
+#include "decode_plan.hpp"
 
 namespace reco {
 

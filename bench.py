@@ -65,7 +65,7 @@ DECODE_TRAFFIC = {
     "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
                 "paper_2608_04771_amd/csrc/decode_attn.hpp", "paper_2608_04771_amd/csrc/decode_plan.hpp",
                 "paper_2608_04771_amd/csrc/decode_plan.cpp"),
-    "sha256": "0008d22a9dc393ea618f5dbdd8db574166e361e4bcaa36d4c869909036853450",
+    "sha256": "4c1219466f72f1d9e5b648e49fdb959bdfe2e01ad937755fb1ddd7405df6826a",
     "workload": "7b-28L-28q4kv-d128-bf16-L16384",
     "fetch_bytes": 555278186,
     "write_bytes": 817152,

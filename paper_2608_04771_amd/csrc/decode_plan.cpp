@@ -12,7 +12,7 @@ namespace reco {
 // split at capacity.  With more units than compute units the grid runs in
 // several rounds anyway; there long units (8K rows or more at capacity) are
 // cut in two, which halves the work of the last workgroups to finish (the
-// ragged 7B batch: 4.49 -> 4.32 ms per call; the 32B 64K batch 12.03 ->
+// ragged 7B batch: 4.49 -> 4.27 ms per call; the 32B 64K batch 12.03 ->
 // 11.91 ms).
 int decode_splits(int units, int capacity, int compute_units) {
   const int tiles_cap = (capacity + 1 + kDecodeTile - 1) / kDecodeTile;

@@ -111,3 +111,25 @@ def assert_theta_precision(s_gpu: np.ndarray, s_or: np.ndarray, L: int, w: int, 
     assert worst <= THETA_RTOL, f"{what}: score rel err near theta {worst:.3e} > {THETA_RTOL:.0e} (theta={theta:.6e})"
     return worst, int(near.sum())
 
+
+def assert_mass_conserved(scores: torch.Tensor, lengths, group: int, w: int, what: str = "", rtol: float = 1e-6,
+                          verbose: bool = True):
+    """Eq. 2 conserves mass: each window row's softmax over the keys it sees
+    sums to one, so the scores of a unit of length L sum to G * min(w, L).
+    Checked on every unit at once (fp64 sums on the device).  The bound 1e-6
+    sits well above the fp32 rounding seen at full size (about 3e-8) and
+    below what losing one key of average weight costs at 64K rows (1/L per
+    row, 1.5e-5).  Returns the largest relative deviation."""
+    L = torch.as_tensor(lengths, device=scores.device).to(torch.int64)
+    cap = scores.shape[-1]
+    mask = torch.arange(cap, device=scores.device) < L[..., None]
+    tot = torch.where(mask, scores.double(), torch.zeros((), dtype=torch.float64, device=scores.device)).sum(-1)
+    expect = (group * torch.clamp(L, max=w)).double()
+    ok = expect > 0
+    dev = ((tot - expect).abs() / expect.clamp(min=1.0))[ok]
+    worst = float(dev.max()) if dev.numel() else 0.0
+    if verbose:
+        print(f"{what}: mass conservation over {int(ok.sum())} units, worst relative deviation {worst:.2e}",
+              flush=True)
+    assert worst <= rtol, f"{what}: scores of a unit do not sum to G*min(w, L) (worst {worst:.3e})"
+    return worst

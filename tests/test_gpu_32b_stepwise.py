@@ -15,16 +15,17 @@ compression, with a retention set by the latest step's reward).
 Every round checks, on sampled units, the scores against the oracle (and the
 near-theta precision), the kept sets (ties excused), the gathered rows bit for
 bit against a snapshot taken before the compression, and decode outputs and
-log-sum-exps at the first and last step; the lengths of all 4,096 units are
-checked after every compression and after the decode steps.  The phase times
-of every round are printed."""
+log-sum-exps at the first and last step; on all 4,096 units it checks the
+lengths and the mass conservation of the scores (each unit's scores sum to
+G * w) after every compression, and the lengths again after the decode steps.
+The phase times of every round are printed."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_theta_precision, f64,
-                         kept_sets_match)
+from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_mass_conserved,
+                         assert_theta_precision, f64, kept_sets_match)
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd import inputs as I
 
@@ -74,6 +75,7 @@ def test_32b_64k_four_rounds_stepwise():
         ev[2].record()
         torch.cuda.synchronize()
         assert dev_err.item() == 0
+        assert_mass_conserved(scores, torch.from_numpy(lens0.astype(np.int64)), G, w, f"round {rnd + 1}")
         score_ms, sel_ms = ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])
         lens1 = cache.length.cpu().numpy()
         for u in np.ndindex(NL, Bsz, H):

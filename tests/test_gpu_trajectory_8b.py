@@ -5,7 +5,9 @@ in reasoning steps of Geometric(mean 200) length, a Beta(2,5) process reward
 and a compression at every step boundary, and the reflection penalty on a
 128,256-token logit row per token.  The oracle checks sampled compressions
 (scores, kept sets with ties excused, bit-exact gathered rows), sampled
-decode outputs, sampled penalised rows and the final lengths."""
+decode outputs, sampled penalised rows and the final lengths; at every
+compression the scores of every unit must sum to G * w (Eq. 2 conserves
+each window row's probability mass)."""
 import math
 import time
 
@@ -14,8 +16,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_theta_precision, f64,
-                         kept_sets_match)
+from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_mass_conserved,
+                         assert_theta_precision, f64, kept_sets_match)
 from paper_2608_04771_amd import inputs as I
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd.controller import RecoDecoder, RecoPolicy
@@ -46,6 +48,7 @@ def test_8b_trajectory_full_size():
     bounds = np.cumsum(steps)
     bi = 0
     checked = {"compress": 0, "decode": 0, "penalty": 0}
+    worst_mass = 0.0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     while tok < wl.decode_steps:
@@ -79,8 +82,12 @@ def test_8b_trajectory_full_size():
                     for u in units:
                         L = int(cache.length[u].item())
                         snap[u] = (L, f64(cache.k[u][:L]), f64(cache.v[u][:L]))
+                L_before = dec.lengths()[0]
                 dec.end_step([float(x) for x in rewards[bi]])
                 band = rewards[bi].astype(np.float32)
+                worst_mass = max(worst_mass, assert_mass_conserved(
+                    dec.scores, torch.full((NL, Bsz, H), L_before, dtype=torch.int64), G, w,
+                    f"8b step {bi}", verbose=False))
                 if check_c:
                     torch.cuda.synchronize()
                     r = oracle.retention_from_reward(float(rewards[bi][0]))
@@ -106,4 +113,5 @@ def test_8b_trajectory_full_size():
     assert (lens == dec.lengths()[0]).all()
     assert checked["compress"] == len(check_bounds) and checked["decode"] == len(check_tokens)
     print(f"8B trajectory: {wl.decode_steps} tokens, {len(steps)} compressions, final cache {lens.max()} rows, "
-          f"{elapsed:.2f} s including input generation and checks")
+          f"{elapsed:.2f} s including input generation and checks; scores of every unit at every compression "
+          f"sum to G*w within {worst_mass:.1e}")

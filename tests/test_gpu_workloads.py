@@ -3,16 +3,17 @@
 The caches are drawn on the GPU with a seeded generator (tens to a hundred GB
 do not fit the host path), every call covers all layers, and the oracle checks
 sampled units by reading them back: scores, kept sets (ties excused),
-bit-exact gathered rows, decode outputs and lse; lengths are checked for every
-unit.  The 32B test also runs the reflection penalty and the answer
+bit-exact gathered rows, decode outputs and lse; lengths and the mass
+conservation of the scores (each unit's scores sum to G * min(w, L)) are
+checked for every unit.  The 32B test also runs the reflection penalty and the answer
 perplexity on its logit shapes."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_theta_precision, f64,
-                         kept_sets_match)
+from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_mass_conserved,
+                         assert_theta_precision, f64, kept_sets_match)
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd import inputs as I
 
@@ -44,6 +45,7 @@ def _run_workload(wl, units, decode_steps, check_steps, seq_lens=None):
     print(f"{wl.name}: score {ev[0].elapsed_time(ev[1]):.2f} ms, select+compact {ev[1].elapsed_time(ev[2]):.2f} ms "
           f"over {int(lens0.sum())} cached rows")
     assert dev_err.item() == 0
+    assert_mass_conserved(scores, torch.from_numpy(lens0.astype(np.int64)), G, wl.window, wl.name)
     m_all = np.array([[oracle.kept_count(int(lens0[0, b, 0]), wl.window, r[b]) for b in range(Bsz)]])
     lens1 = cache.length.cpu().numpy()
     assert (lens1 == m_all[:, :, None]).all()

@@ -133,3 +133,37 @@ def assert_mass_conserved(scores: torch.Tensor, lengths, group: int, w: int, wha
               flush=True)
     assert worst <= rtol, f"{what}: scores of a unit do not sum to G*min(w, L) (worst {worst:.3e})"
     return worst
+
+
+def assert_decode_all_units(cache, q: torch.Tensor, out: torch.Tensor, lse: torch.Tensor, n_rows, scale: float,
+                            what: str = ""):
+    """Every unit of a full-size decode call against a plain PyTorch fp32
+    attention on the device (a cross-check of all units; the fp64 oracle
+    checks sampled units): softmax(scale * q K^T) V over the first n rows of
+    each unit, GQA groups G = Hq / Hkv.  `n_rows` [NL][B][H] is the number of
+    rows each unit attended (the appended one included).  bf16 outputs within
+    2e-2, lse within 1e-4."""
+    NL, Bsz, H, Cap, D = cache.k.shape
+    Hq = q.shape[2]
+    G = Hq // H
+    n = torch.as_tensor(n_rows, device=q.device).to(torch.int64)
+    worst_o = worst_l = 0.0
+    for l in range(NL):
+        nmax = int(n[l].max().item())
+        K = cache.k[l, :, :, :nmax].float()                       # [B][H][n][D]
+        V = cache.v[l, :, :, :nmax].float()
+        ql = q[l].float().reshape(Bsz, H, G, D)
+        s = torch.matmul(ql, K.transpose(-1, -2).contiguous()) * scale   # [B][H][G][n]
+        keep = torch.arange(nmax, device=q.device)[None, None, None, :] < n[l][:, :, None, None]
+        s = s.masked_fill(~keep, float("-inf"))
+        ref_lse = torch.logsumexp(s, dim=-1)                              # [B][H][G]
+        ref_out = torch.matmul(torch.softmax(s, dim=-1), V)               # [B][H][G][D]
+        o = out[l].float().reshape(Bsz, H, G, D)
+        z = lse[l].reshape(Bsz, H, G)
+        worst_o = max(worst_o, float((o - ref_out).abs().max()))
+        worst_l = max(worst_l, float((z - ref_lse).abs().max()))
+        del K, V, s
+    print(f"{what}: all {NL * Bsz * H} units against fp32 attention: out {worst_o:.2e}, lse {worst_l:.2e}",
+          flush=True)
+    assert worst_o <= 2e-2, f"{what}: decode output off by {worst_o:.3e}"
+    assert worst_l <= 1e-4, f"{what}: lse off by {worst_l:.3e}"

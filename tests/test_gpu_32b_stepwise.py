@@ -17,15 +17,16 @@ near-theta precision), the kept sets (ties excused), the gathered rows bit for
 bit against a snapshot taken before the compression, and decode outputs and
 log-sum-exps at the first and last step; on all 4,096 units it checks the
 lengths and the mass conservation of the scores (each unit's scores sum to
-G * w) after every compression, and the lengths again after the decode steps.
-The phase times of every round are printed."""
+G * w) after every compression, the lengths again after the decode steps,
+and the last decode call of each round against a plain PyTorch fp32
+attention on the device.  The phase times of every round are printed."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_mass_conserved,
-                         assert_theta_precision, f64, kept_sets_match)
+from gpu_helpers import (SCORE_RTOL, assert_decode_all_units, assert_decode_close, assert_lse_close,
+                         assert_mass_conserved, assert_theta_precision, f64, kept_sets_match)
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd import inputs as I
 
@@ -104,6 +105,9 @@ def test_32b_64k_four_rounds_stepwise():
                 if s == steps - 1:
                     ev[4].record()
                 torch.cuda.synchronize()
+                if s == steps - 1:
+                    assert_decode_all_units(cache, qs[s], out, lse, torch.from_numpy(lens1.astype(np.int64)) + s + 1,
+                                            scale, f"round {rnd + 1} step {s}")
                 for u in UNITS:
                     l, b, h = u
                     n = int(lens1[u]) + s + 1                        # the call appended row n - 1

@@ -5,15 +5,16 @@ do not fit the host path), every call covers all layers, and the oracle checks
 sampled units by reading them back: scores, kept sets (ties excused),
 bit-exact gathered rows, decode outputs and lse; lengths and the mass
 conservation of the scores (each unit's scores sum to G * min(w, L)) are
-checked for every unit.  The 32B test also runs the reflection penalty and the answer
-perplexity on its logit shapes."""
+checked for every unit, and the decode outputs and lse of every unit
+against a plain PyTorch fp32 attention on the device.  The 32B test also
+runs the reflection penalty and the answer perplexity on its logit shapes."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from gpu_helpers import (SCORE_RTOL, assert_decode_close, assert_lse_close, assert_mass_conserved,
-                         assert_theta_precision, f64, kept_sets_match)
+from gpu_helpers import (SCORE_RTOL, assert_decode_all_units, assert_decode_close, assert_lse_close,
+                         assert_mass_conserved, assert_theta_precision, f64, kept_sets_match)
 from paper_2608_04771_amd import binding as B
 from paper_2608_04771_amd import inputs as I
 
@@ -71,6 +72,8 @@ def _run_workload(wl, units, decode_steps, check_steps, seq_lens=None):
         if s in check_steps:
             torch.cuda.synchronize()
             assert torch.isfinite(out.float()).all()
+            assert_decode_all_units(cache, qs[s], out, lse, torch.from_numpy(lens1.astype(np.int64)) + s + 1,
+                                    scale, f"{wl.name} step {s}")
             for u in units:
                 n = int(lens1[u]) + s + 1
                 l, b, h = u

@@ -924,11 +924,11 @@ def run_trajectory(args, wl, dev):
                "capacity": TRAJ_CAP})
 
 
-def cpu_baseline_trajectory(wl, ci, k0, v0, prompt, qa, ka, va, bounds, rewards, w, budget_s: float = 12.0):
+def cpu_baseline_trajectory(wl, ci, k0, v0, prompt, qa, ka, va, bounds, rewards, w, budget_s: float = 25.0):
     """The oracle runs the trajectory from the prompt (decode with append on
     every token, Eq. 2 compression of every unit at each step boundary) until
-    its time budget is used; the rate is the KV tokens it processed over the
-    time it took."""
+    its time budget is used or 2,048 tokens are generated; the rate is the KV
+    tokens it processed over the time it took."""
     import oracle
     from threadpoolctl import threadpool_limits, threadpool_info
     NL, Bsz, H, _, D = ci.k.shape
@@ -947,7 +947,7 @@ def cpu_baseline_trajectory(wl, ci, k0, v0, prompt, qa, ka, va, bounds, rewards,
     bi = 0
     with threadpool_limits(limits=threads):
         cores = max([p_.get("num_threads", 1) for p_ in threadpool_info()] + [1])
-        while t_used < budget_s and tok < min(4096, qa.shape[0]):
+        while t_used < budget_s and tok < min(2048, qa.shape[0]):
             q, kn, vn = I.to_f64(qa[tok]), I.to_f64(ka[tok]), I.to_f64(va[tok])
             c0, t0 = time.process_time(), time.perf_counter()
             oracle.decode_cache(K, V, lens, q, scale, kn, vn)
@@ -1073,6 +1073,8 @@ def main():
         "phase_ms": {"score": float(score_ms.mean()), "select_compact": float(sel_ms.mean()),
                      "compress": float(comp_ms.mean()), "decode_call": dec_avg_ms,
                      "decode_calls_total": float(dec_loop_ms.mean()), "answer_ppl": float(ppl_ms.mean())},
+        "answer_ppl": {"ms": float(ppl_ms.mean()), "logit_bytes": ab["ppl"],
+                       "GBps": ab["ppl"] / (float(ppl_ms.mean()) * 1e-3) / 1e9},
         "score_after_decode": score_fed,
         "decode_per_layer_graph": per_layer,
         "penalty_sample": {"ms_per_step": float(smp_ms.mean()), "rows_per_step": int(w.tokens.numel()),

@@ -287,7 +287,7 @@ __global__ __launch_bounds__(kPplThreads) void ppl_final_kernel(const float *log
   red[threadIdx.x] = bad ? NAN : nll;
   __syncthreads();
   for (int s = kPplThreads / 2; s > 0; s >>= 1) {
-    if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    if (static_cast<int>(threadIdx.x) < s) red[threadIdx.x] += red[threadIdx.x + s];
     __syncthreads();
   }
   if (threadIdx.x == 0) {

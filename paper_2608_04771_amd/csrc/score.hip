@@ -650,7 +650,7 @@ __device__ V2Run v2_run(const ScoreParams &p, long long *scan) {
   __syncthreads();
   // Inclusive scan (Hillis-Steele) over the thread totals.
   for (int off = 1; off < kV2Threads; off <<= 1) {
-    const long long v = threadIdx.x >= off ? scan[threadIdx.x - off] : 0;
+    const long long v = static_cast<int>(threadIdx.x) >= off ? scan[threadIdx.x - off] : 0;
     __syncthreads();
     scan[threadIdx.x] += v;
     __syncthreads();

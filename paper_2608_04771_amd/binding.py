@@ -381,6 +381,65 @@ def reco_decode_attn_noalloc(cache: KVCache, q: torch.Tensor, out: torch.Tensor,
     return out, lse
 
 
+class PreparedDecode:
+    """reco_decode_attn for a loop that calls it again and again with the same
+    cache, outputs, workspace and error word (a decoder's per-token call):
+    those are checked once here, and each call checks only the tensors that
+    change from token to token (query, new K/V rows, statistics slot) against
+    the shapes fixed at construction before passing their pointers on.  The
+    library computes exactly what reco_decode_attn computes."""
+
+    def __init__(self, cache: KVCache, n_q_heads: int, out: torch.Tensor, lse: Optional[torch.Tensor],
+                 ws: torch.Tensor, dev_err: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+                 layer0: int = 0, n_layers: Optional[int] = None):
+        layer0, nl = _layers(cache, layer0, n_layers)
+        NL, Bsz, H, Cap, D = cache.shape
+        hq = int(n_q_heads)
+        if out is None or ws is None:
+            raise ValueError("out and ws must be given")
+        _expect(out, "out", (nl, Bsz, hq, D), cache.k.dtype)
+        _expect(lse, "lse", (nl, Bsz, hq), torch.float32)
+        _expect_dev_err(dev_err)
+        _need_cuda(cache.k, out, lse, ws, dev_err)
+        _same_gpu(out, cache.k)
+        if _nbytes(ws) < decode_attn_workspace_size(cache, hq, nl):
+            raise ValueError("ws is smaller than reco_decode_attn_workspace_size")
+        self.cache, self.out, self.lse, self.ws, self.dev_err = cache, out, lse, ws, dev_err
+        self._fn = load_library().reco_decode_attn
+        self._dev = cache.k.device
+        self._dt = cache.k.dtype
+        self._q_shape = (nl, Bsz, hq, D)
+        self._kv_shape = (nl, Bsz, H, D)
+        self._st_shape = (nl, Bsz, hq, 2)
+        self._fixed_head = (cache.ref(), layer0, nl)
+        self._hq = hq
+        self._scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+        self._fixed_tail = (_ptr(out), _ptr(lse))
+        self._ws = (_ptr(ws), _nbytes(ws), _ptr(dev_err))
+
+    def _check_t(self, t: torch.Tensor, what: str, shape, dtype: torch.dtype):
+        if (tuple(t.shape) != shape or t.dtype != dtype or t.device != self._dev or not t.is_contiguous()):
+            raise ValueError(f"{what} must be a contiguous {_DT.get(dtype, dtype)} {list(shape)} tensor on "
+                             f"{self._dev}")
+
+    def __call__(self, q: torch.Tensor, k_new: Optional[torch.Tensor] = None, v_new: Optional[torch.Tensor] = None,
+                 row_stats: Optional[torch.Tensor] = None):
+        self._check_t(q, "q", self._q_shape, self._dt)
+        if (k_new is None) != (v_new is None):
+            raise ValueError("k_new and v_new must be given together")
+        if k_new is not None:
+            self._check_t(k_new, "k_new", self._kv_shape, self._dt)
+            self._check_t(v_new, "v_new", self._kv_shape, self._dt)
+        if row_stats is not None:
+            self._check_t(row_stats, "row_stats", self._st_shape, torch.float32)
+        cref, layer0, nl = self._fixed_head
+        st = self._fn(cref, layer0, nl, _ptr(q), self._hq, self._scale, _ptr(k_new), _ptr(v_new),
+                      *self._fixed_tail, _ptr(row_stats), *self._ws, _stream(self._dev))
+        if st != RECO_OK:
+            _check(st, "reco_decode_attn")
+        return self.out, self.lse
+
+
 def _logit_rows(logits: torch.Tensor):
     if logits.dtype != torch.float32 or logits.dim() != 2 or logits.stride(1) != 1 or \
             logits.stride(0) < logits.shape[1]:
@@ -431,6 +490,49 @@ def reco_penalty_sample(logits: torch.Tensor, refl_ids: Optional[torch.Tensor], 
                                             _ptr(dev_err), _stream(logits.device))
     _check(st, "reco_penalty_sample")
     return tokens
+
+
+class PreparedPenaltySample:
+    """reco_penalty_sample for a loop over logit rows of one shape (a
+    decoder's per-token draw): the reflection ids, the per-row rewards, the
+    token output, the workspace and the error word are checked once, and each
+    call checks only the logit rows before passing their pointer on, with
+    the temperature, seed and draw offset of that call."""
+
+    def __init__(self, rows: int, vocab: int, refl_ids: Optional[torch.Tensor], reward: torch.Tensor,
+                 tokens: torch.Tensor, ws: torch.Tensor, dev_err: Optional[torch.Tensor] = None):
+        rows, vocab = int(rows), int(vocab)
+        if refl_ids is not None and (refl_ids.dtype != torch.int32 or refl_ids.dim() != 1):
+            raise ValueError("refl_ids must be a 1-D int32 tensor")
+        if tokens is None or ws is None:
+            raise ValueError("tokens and ws must be given")
+        _expect(reward, "reward", (rows,), torch.float32)
+        _expect(tokens, "tokens", (rows,), torch.int32)
+        _expect_dev_err(dev_err)
+        _need_cuda(reward, refl_ids, tokens, ws, dev_err)
+        _same_gpu(tokens, reward)
+        if _nbytes(ws) < penalty_sample_workspace_size(rows, vocab):
+            raise ValueError("ws is smaller than reco_penalty_sample_workspace_size")
+        self.tokens = tokens
+        self._keep = (refl_ids, reward, ws, dev_err)
+        self._fn = load_library().reco_penalty_sample
+        self._dev = reward.device
+        self._rows, self._vocab = rows, vocab
+        self._ids = (_ptr(refl_ids), 0 if refl_ids is None else refl_ids.numel(), _ptr(reward))
+        self._tail = (_ptr(tokens), _ptr(ws), _nbytes(ws), _ptr(dev_err))
+
+    def __call__(self, logits: torch.Tensor, tau_lo: float, tau_hi: float, beta_lo: float, beta_mid: float,
+                 beta_hi: float, temperature: float, seed: int, offset: int) -> torch.Tensor:
+        if (logits.dtype != torch.float32 or logits.dim() != 2 or tuple(logits.shape) != (self._rows, self._vocab)
+                or logits.stride(1) != 1 or logits.stride(0) < self._vocab or logits.device != self._dev):
+            raise ValueError(f"logits must be fp32 [{self._rows}][{self._vocab}] with unit column stride on "
+                             f"{self._dev}")
+        st = self._fn(_ptr(logits), self._rows, self._vocab, logits.stride(0), *self._ids, tau_lo, tau_hi, beta_lo,
+                      beta_mid, beta_hi, float(temperature), int(seed) & (2 ** 64 - 1), int(offset) & (2 ** 64 - 1),
+                      *self._tail, _stream(self._dev))
+        if st != RECO_OK:
+            _check(st, "reco_penalty_sample")
+        return self.tokens
 
 
 def reco_answer_ppl(logits: torch.Tensor, tokens: torch.Tensor, tau_p: float, ppl: Optional[torch.Tensor] = None,

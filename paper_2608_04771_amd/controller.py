@@ -29,8 +29,10 @@ compression trigger, probe trigger) and runs without a GPU.  `RecoDecoder`
 drives the kernels through the binding: it keeps the window queries in a ring
 buffer on the device, calls reco_decode_attn and reco_logit_penalty (or the
 fused reco_penalty_sample) per token and reco_score / reco_select_compact at
-step boundaries.  All arithmetic of
-the method runs in the library; this module decides when, and moves data.
+step boundaries.  The two per-token calls go through the binding's prepared
+forms, which check the decoder's fixed buffers once and each token's tensors
+on every call.  All arithmetic of the method runs in the library; this
+module decides when, and moves data.
 """
 from __future__ import annotations
 
@@ -169,6 +171,9 @@ class RecoDecoder:
         shift = prompt_len % w
         if shift:
             self.ring = torch.roll(self.ring, shifts=shift, dims=0).contiguous()
+        # The per-token calls, with their fixed buffers checked once here.
+        self._decode_call = B.PreparedDecode(cache, n_q_heads, self.out, self.lse, self.ws_dec, self.dev_err)
+        self._sample_call = None
 
     def query_slot(self) -> torch.Tensor:
         """The ring slot of the next token's query, [NL][B][Hq][D]: a caller
@@ -184,9 +189,10 @@ class RecoDecoder:
         w = self.policy.window
         slot = self.ring[self.count % w]
         if q.data_ptr() != slot.data_ptr():
+            if tuple(q.shape) != tuple(slot.shape) or q.dtype != slot.dtype or q.device != slot.device:
+                raise ValueError(f"q must be {list(slot.shape)} {slot.dtype} on {slot.device}")
             slot.copy_(q)
-        B.reco_decode_attn(self.cache, slot, k_new, v_new, out=self.out, lse=self.lse, ws=self.ws_dec,
-                           dev_err=self.dev_err, row_stats=self.stats_ring[self.count % w])
+        self._decode_call(slot, k_new, v_new, self.stats_ring[self.count % w])
         if logits is not None and self.refl is not None:
             p = self.policy
             B.reco_logit_penalty(logits, self.refl, self.band_reward, p.tau_lo, p.tau_hi, *p.betas,
@@ -204,15 +210,18 @@ class RecoDecoder:
         Returns the tokens [B] int32 (a buffer reused by the next call)."""
         if self.refl is None:
             raise ValueError("sampling with the reflection penalty needs refl_ids")
+        if logits.dim() != 2:
+            raise ValueError("logits must be [B][vocab]")
         rows, vocab = logits.shape
         if self.smp_shape != (rows, vocab):
             need = B.penalty_sample_workspace_size(rows, vocab)
             if self.ws_smp is None or self.ws_smp.numel() < need:
                 self.ws_smp = torch.empty(need, dtype=torch.uint8, device=logits.device)
+            self._sample_call = B.PreparedPenaltySample(rows, vocab, self.refl, self.band_reward, self.tokens,
+                                                        self.ws_smp, self.dev_err)
             self.smp_shape = (rows, vocab)
         p = self.policy
-        return B.reco_penalty_sample(logits, self.refl, self.band_reward, p.tau_lo, p.tau_hi, *p.betas, temperature,
-                                     seed, self.count, tokens=self.tokens, ws=self.ws_smp, dev_err=self.dev_err)
+        return self._sample_call(logits, p.tau_lo, p.tau_hi, *p.betas, temperature, seed, self.count)
 
     def window_queries(self) -> torch.Tensor:
         """The last w queries in order (row t = position L - w + t)."""

@@ -132,3 +132,30 @@ def test_answer_ppl_arguments():
     _raises("ppl", B.reco_answer_ppl, z, tok, 1.1, ppl=_z(1))
     _raises("stop", B.reco_answer_ppl, z, tok, 1.1, stop=_z(2))
     _raises("GPU", B.reco_answer_ppl, z, tok, 1.1, ppl=_z(2), stop=_z(2, dtype=I32))
+
+
+def test_prepared_decode_checks_its_fixed_buffers():
+    c = _cache()
+    out = _z(NL, BS, HQ, D, dtype=BF)
+    lse = _z(NL, BS, HQ)
+    ws = _z(1 << 20, dtype=torch.uint8)
+    _raises("out", B.PreparedDecode, c, HQ, _z(NL, BS, HQ, D), lse, ws)                 # wrong dtype
+    _raises("out", B.PreparedDecode, c, HQ, _z(NL, BS, HQ - 1, D, dtype=BF), lse, ws)
+    _raises("lse", B.PreparedDecode, c, HQ, out, _z(NL, BS, HQ + 1), ws)
+    _raises("dev_err", B.PreparedDecode, c, HQ, out, lse, ws, dev_err=_z(1, dtype=torch.int64))
+    _raises("must be given", B.PreparedDecode, c, HQ, out, lse, None)
+    _raises("layers", B.PreparedDecode, c, HQ, out, lse, ws, layer0=2)
+    _raises("GPU", B.PreparedDecode, c, HQ, out, lse, ws)
+
+
+def test_prepared_penalty_sample_checks_its_fixed_buffers():
+    rows, vocab = 4, 1000
+    ids = _z(8, dtype=I32)
+    rew = _z(rows)
+    tok = _z(rows, dtype=I32)
+    ws = _z(1 << 16, dtype=torch.uint8)
+    _raises("refl_ids", B.PreparedPenaltySample, rows, vocab, _z(8), rew, tok, ws)
+    _raises("reward", B.PreparedPenaltySample, rows, vocab, ids, _z(rows + 1), tok, ws)
+    _raises("tokens", B.PreparedPenaltySample, rows, vocab, ids, rew, _z(rows, dtype=torch.int64), ws)
+    _raises("must be given", B.PreparedPenaltySample, rows, vocab, ids, rew, tok, None)
+    _raises("GPU", B.PreparedPenaltySample, rows, vocab, ids, rew, tok, ws)

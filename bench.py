@@ -512,6 +512,9 @@ def E():
 # ---------------------------------------------------------------------------
 
 def run_batch(args, wl, dev):
+    """The ragged 7B batch: one compression (score, select, compact) and 256
+    decode calls over all layers per step, from a working cache copied back
+    from a pristine copy between steps (untimed)."""
     ci = I.make_cache(wl, device=dev)                           # the pristine cache
     NL, Bsz, H, Cap, D = ci.k.shape
     e, Hq, w = wl.elem_bytes, wl.n_q_heads, wl.window
@@ -623,6 +626,10 @@ ROUNDS_32B = 4
 
 
 def run_32b(args, wl, dev):
+    """The 32B-shaped batch: four rounds of (compression -> 64 decode calls,
+    the round's logit rows penalised and sampled on a side stream), rounds
+    2-4 scored in one pass with the decode statistics, then the answer probe;
+    the cache is regenerated from its seed between steps (untimed)."""
     steps, w, G, V = wl.decode_steps, wl.window, wl.group, wl.vocab
     cap = int(wl.lengths[0]) + ROUNDS_32B * steps
     state = {"ci": None}
@@ -802,6 +809,10 @@ PROBE_REPEATS = 8
 
 
 def run_trajectory(args, wl, dev):
+    """The 8B-shaped trajectory through the controller: a 512-token prompt
+    and 32,768 generated tokens (decode, penalty and draw per token, a
+    compression at every step boundary), every token's inputs staged in HBM
+    beforehand and the prompt restored between steps (untimed)."""
     from paper_2608_04771_amd.controller import RecoDecoder, RecoPolicy
     T, w, V = wl.decode_steps, wl.window, wl.vocab
     ci = I.make_cache(wl, device=dev, capacity=TRAJ_CAP)

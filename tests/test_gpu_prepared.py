@@ -70,3 +70,48 @@ def test_prepared_penalty_sample_matches_reco_penalty_sample():
         call(torch.zeros((rows, vocab - 1), device=dev), 0.4, 0.8, 0.0, 1.0, 3.0, 1.0, 99, 0)
     with pytest.raises(ValueError, match="logits must be"):
         call(torch.zeros((rows, vocab), device=dev, dtype=torch.float64), 0.4, 0.8, 0.0, 1.0, 3.0, 1.0, 99, 0)
+
+
+def test_prepared_decode_in_a_graph_replays_match_eager():
+    """Per-layer prepared calls (no append) captured in a HIP graph: every
+    replay, with eager work between replays, equals the eager calls bit for
+    bit."""
+    wl = I.WORKLOADS["7b16k"]
+    dev = torch.device("cuda")
+    ci = I.make_cache(wl, device=dev, n_layers=4, seq_lens=[2500])
+    cache = B.KVCache(ci.k, ci.v, ci.length)
+    NL, Bsz, H, Cap, D = cache.shape
+    Hq = wl.n_q_heads
+    g = torch.Generator(device="cuda").manual_seed(11)
+    q = torch.randn((NL, Bsz, Hq, D), device=dev, generator=g).to(torch.bfloat16)
+    ws = torch.empty(B.decode_attn_workspace_size(cache, Hq, 1), dtype=torch.uint8, device=dev)
+    out = torch.empty_like(q)
+    lse = torch.empty((NL, Bsz, Hq), dtype=torch.float32, device=dev)
+    calls = [B.PreparedDecode(cache, Hq, out[l:l + 1], lse[l:l + 1], ws, layer0=l, n_layers=1) for l in range(NL)]
+
+    def per_layer():
+        for l in range(NL):
+            calls[l](q[l:l + 1])
+
+    per_layer()
+    torch.cuda.synchronize()
+    ref_out, ref_lse = out.clone(), lse.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        per_layer()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        per_layer()
+    for rep in range(3):
+        out.zero_()
+        lse.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref_out), f"replay {rep}: out differs"
+        assert torch.equal(lse, ref_lse), f"replay {rep}: lse differs"
+        B.reco_decode_attn(cache, q)                                # eager work between replays
+        torch.cuda.synchronize()
+    assert (cache.length.cpu().numpy() == 2500).all()

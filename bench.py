@@ -56,19 +56,23 @@ SAMPLE_SEED = 0x5EED
 N_REFL = 64
 ANSWER_LEN = 32
 
-# HBM traffic of one decode_split_kernel launch on this workload, from two
+# HBM traffic of one decode_split_kernel launch per workload, from two
 # rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE), each scaled by what the
 # counter reads for a plain device copy of known size (factors 0.5001 and
-# 1.0000).  Valid only for the kernel sources it was taken with: if those
-# files change, the figure is reported as null until it is measured again.
+# 1.0000, taken in the 7B 16K run, whose bench stages such copies).  Valid
+# only for the kernel sources it was taken with: if those files change, the
+# figure is reported as null until it is measured again.
 DECODE_TRAFFIC = {
     "sources": ("paper_2608_04771_amd/csrc/decode_attn.hip", "paper_2608_04771_amd/csrc/reco_device.hpp",
                 "paper_2608_04771_amd/csrc/decode_attn.hpp", "paper_2608_04771_amd/csrc/decode_plan.hpp",
                 "paper_2608_04771_amd/csrc/decode_plan.cpp"),
     "sha256": "4c1219466f72f1d9e5b648e49fdb959bdfe2e01ad937755fb1ddd7405df6826a",
-    "workload": "7b-28L-28q4kv-d128-bf16-L16384",
-    "fetch_bytes": 555278186,
-    "write_bytes": 817152,
+    # (fetched, written) bytes per decode_split_kernel dispatch, mean over a timed step's calls
+    "per_workload": {
+        "7b-28L-28q4kv-d128-bf16-L16384": (555278186, 817152),
+        "7b-28L-28q4kv-d128-bf16-B32-L4k-32k": (27506962867, 26149806),
+        "32b-64L-40q8kv-d128-bf16-B8-L65536": (78520722242, 21497514),
+    },
 }
 
 
@@ -78,9 +82,10 @@ def decode_traffic(workload_name: str):
     for f in DECODE_TRAFFIC["sources"]:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
-    if h.hexdigest() != DECODE_TRAFFIC["sha256"] or workload_name != DECODE_TRAFFIC["workload"]:
+    per = DECODE_TRAFFIC["per_workload"].get(workload_name)
+    if h.hexdigest() != DECODE_TRAFFIC["sha256"] or per is None:
         return None
-    return DECODE_TRAFFIC["fetch_bytes"] + DECODE_TRAFFIC["write_bytes"]
+    return per[0] + per[1]
 
 
 def log(msg):
@@ -569,7 +574,8 @@ def run_batch(args, wl, dev):
                      "select_compact": float(np.mean([ev["c1"].elapsed_time(ev["c2"]) for ev in evs])),
                      "decode_call": float(dec_ms.mean()),
                      "decode_calls_total": float(np.mean([ev["c2"].elapsed_time(ev["d1"]) for ev in evs]))},
-        "roofline": roofline_obj(DECODE_KERNELS, float(np.mean(dec)), float(dec_ms.mean())),
+        "roofline": roofline_obj(DECODE_KERNELS, float(np.mean(dec)), float(dec_ms.mean()),
+                                 traffic=decode_traffic(wl.name)),
     }
     if args.cpu_baseline:
         log("timing the CPU oracle on sampled units")
@@ -754,7 +760,8 @@ def run_32b(args, wl, dev):
         "rounds": round_info,
         "phase_ms": {"answer_ppl": float(np.mean([ev["p0"].elapsed_time(ev["p1"]) for ev in evs])),
                      "decode_call": dec_avg_ms},
-        "roofline": roofline_obj(DECODE_KERNELS, float(np.mean(dec_bytes_all)), dec_avg_ms),
+        "roofline": roofline_obj(DECODE_KERNELS, float(np.mean(dec_bytes_all)), dec_avg_ms,
+                                 traffic=decode_traffic(wl.name)),
     }
     if args.cpu_baseline:
         log("timing the CPU oracle on sampled units")
